@@ -1,0 +1,205 @@
+#!/usr/bin/env python3
+"""Packed-prefill benchmark on one MI355X.
+
+A step is one pp_prefill call: the whole device path (TENSORIZE, every decoder layer under
+the independent mask with restart positions, KV and hidden-state UNPACK) over one batch of
+synthetic prompts, with weights, tokens and the device plan already resident in HBM.
+pp_pack (host) and the plan upload are timed separately and never part of `value`.
+
+Prints one JSON line:
+  value            effective (non-pad) prefill tokens/s of the packed path
+  tflops_effective algorithmic FLOP / time (pads and skipped work excluded)
+  padded           the same kernels on the full-batching plan (the paper's baseline)
+  roofline         the dominant kernel (the gate/up projection GEMM with SwiGLU epilogue),
+                   timed live with HIP events on its stream, against the bf16 MFMA peak
+  cpu_baseline     the CPU oracle timed on a bounded sample of the same workload
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+METRIC = "effective prefill tokens/s + TFLOP/s (% bf16 MFMA peak) vs padded prefill"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_flops(shape, lengths):
+    """Linear layers of every real token plus causal attention pairs; norms, RoPE, softmax = 0."""
+    import numpy as np
+    s = shape
+    L = int(np.sum(lengths))
+    lin = 2 * (s.d_model * (s.n_heads + 2 * s.n_kv_heads) * s.head_dim + s.n_heads * s.head_dim * s.d_model
+               + 3 * s.d_model * s.ffn_dim)
+    pairs = int(np.sum(np.asarray(lengths, dtype=np.int64) * (np.asarray(lengths, dtype=np.int64) + 1) // 2))
+    return s.n_layers * (L * lin + 4 * s.n_heads * s.head_dim * pairs)
+
+
+def time_steps(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = sorted(a.elapsed_time(b) for a, b in ev)
+    return {"ms_mean": sum(ms) / len(ms), "ms_median": ms[len(ms) // 2], "ms_p10": ms[len(ms) // 10],
+            "ms_p90": ms[min(len(ms) - 1, (9 * len(ms)) // 10)], "wall_s": wall}
+
+
+def cpu_baseline(case, budget_s):
+    """The oracle (float64, per prompt, as it stands) on prompts of the workload taken in
+    original order, skipping prompts longer than 512 tokens, until budget_s has elapsed."""
+    import numpy as np
+    from oracle import decoder as D
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        cores = 1
+    shape = D.Shape.of(case.shape)
+    off = np.concatenate([[0], np.cumsum(case.lengths)])
+    done, t0, used = 0, time.perf_counter(), []
+    for i, l in enumerate(case.lengths):
+        if l > 512:
+            continue
+        D.prefill_prompt(case.tokens[off[i]:off[i + 1]], case.weights, shape)
+        done += int(l)
+        used.append(i)
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": done / el, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{len(used)} prompts ({done} tokens) of the same batch in original order, prompts "
+                      f"longer than 512 tokens skipped; float64 numpy oracle, all {shape.n_layers} layers; "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2, help="workload id (2 = Llama-2-7B shape, lognormal)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-padded", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--kernel-launches", type=int, default=20)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the packed prefill is a single-GPU path (rows are independent, "
+              "so it would shard by rows with no collective); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2404_09529_amd import prepack as pp
+    from paper_2404_09529_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    pp.lib()
+    torch.cuda.set_device(0)
+
+    t = time.perf_counter()
+    case = W.make_case(args.workload, args.seed)
+    shape, lengths = case.shape, case.lengths
+    log(f"workload {case.wl.name}: k={len(lengths)} L={case.total_len} m={lengths.max()} "
+        f"(weights drawn in {time.perf_counter() - t:.1f} s)")
+
+    # host planning, timed on its own
+    n_pack = 50
+    t = time.perf_counter()
+    for _ in range(n_pack):
+        plan = pp.pp_pack(lengths, case.capacity)
+    pack_ms = (time.perf_counter() - t) * 1e3 / n_pack
+    t = time.perf_counter()
+    dplan = pp.DevicePlan(plan)
+    torch.cuda.synchronize()
+    upload_ms = (time.perf_counter() - t) * 1e3
+    model = pp.DeviceModel(shape, case.weights)
+    tokens = torch.from_numpy(case.tokens).cuda()
+    step = pp.Prefill(model, dplan)
+    log(f"packed plan: {plan.n_rows} rows x {plan.capacity}, fill {case.total_len / plan.n_slots:.3f}, "
+        f"pack {pack_ms:.3f} ms, upload {upload_ms:.2f} ms")
+
+    flops = algorithmic_flops(shape, lengths)
+    packed = time_steps(lambda: step(tokens), args.steps, args.warmup)
+    ms = packed["ms_mean"]
+    value = case.total_len / (ms / 1e3)
+    tflops = flops / (ms / 1e3) / 1e12
+    log(f"packed: {ms:.3f} ms/step, {value:,.0f} tokens/s, {tflops:.1f} TFLOP/s effective")
+
+    # dominant kernel: the gate/up GEMM with the SwiGLU epilogue, same launch as inside pp_prefill
+    T, d, F = plan.n_slots, shape.d_model, shape.ffn_dim
+    gen = torch.Generator(device="cuda").manual_seed(1)
+    A = torch.randn((T, d), generator=gen, device="cuda").to(torch.bfloat16)
+    Cb = torch.empty((T, F), dtype=torch.bfloat16, device="cuda")
+    Wgu = model.layers[0]["w_gateup"]
+    kstream = torch.cuda.current_stream()
+    gemm = lambda: pp.pp_gemm(pp.PP_BF16, pp.PP_EPI_SWIGLU, A, d, Wgu, d, Cb, F, T, 2 * F, d, dplan, kstream)
+    kt = time_steps(gemm, args.kernel_launches, 3)
+    k_flops = 2.0 * case.total_len * (2 * F) * d
+    achieved = k_flops / (kt["ms_mean"] / 1e3) / 1e12
+    del A, Cb
+    log(f"gate/up GEMM: {kt['ms_mean']:.3f} ms/launch, {achieved:.1f} TFLOP/s algorithmic")
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
+        "config": {"workload": case.wl.name, "description": case.wl.description, "seed": args.seed,
+                   "k": int(len(lengths)), "capacity": int(case.capacity), "total_len": case.total_len,
+                   "max_len": int(lengths.max()), "n_rows": plan.n_rows, "fill": round(case.total_len / plan.n_slots, 4)},
+        "tflops_effective": round(tflops, 2), "frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "algorithmic_flop": flops,
+        "ms_median": round(packed["ms_median"], 4), "ms_p10": round(packed["ms_p10"], 4),
+        "ms_p90": round(packed["ms_p90"], 4),
+        "pack_ms": round(pack_ms, 4), "plan_upload_ms": round(upload_ms, 3),
+        "roofline": {"kernel": "gemm_bf16_kernel<kSwiGLU> (gate/up projection)", "bound": "mfma",
+                     "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "ms_per_launch": round(kt["ms_mean"], 4),
+                     "algorithmic_flop_per_launch": k_flops},
+    }
+    del step
+    torch.cuda.empty_cache()
+
+    if not args.no_padded:
+        pplan = pp.pp_pack_padded(lengths)
+        pstep = pp.Prefill(model, pp.DevicePlan(pplan))
+        padded = time_steps(lambda: pstep(tokens), max(3, args.steps // 4), 1)
+        pms = padded["ms_mean"]
+        out["padded"] = {"ms_per_step": round(pms, 4), "tokens_per_s": round(case.total_len / (pms / 1e3), 1),
+                         "tflops_effective": round(flops / (pms / 1e3) / 1e12, 2), "n_rows": pplan.n_rows,
+                         "capacity": pplan.capacity}
+        out["speedup_vs_padded"] = round(pms / ms, 3)
+        log(f"padded: {pms:.3f} ms/step, speedup {pms / ms:.2f}x")
+        del pstep
+        torch.cuda.empty_cache()
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(case, args.cpu_budget_s)
+        log(f"cpu oracle: {out['cpu_baseline']['value']:.1f} tokens/s on {out['cpu_baseline']['cores']} threads")
+
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

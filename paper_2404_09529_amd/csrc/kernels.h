@@ -1,0 +1,61 @@
+// Host-side launchers of the gfx950 kernels (one translation unit per kernel family).
+// Element types: dtype == PP_F32 -> float, PP_BF16 -> __bf16.  All launches are
+// asynchronous on `s`; callers check hipGetLastError once after enqueuing.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ppk {
+
+// cos/sin(p * theta^(-2i/D)) for p < P, i < D/2, evaluated in float64, stored float2 [P][D/2].
+void rope_table(float2* table, int P, int D, float theta, hipStream_t s);
+
+// x[t] = E[tokens[slot_kv[t]]] (float32), or 0 where slot_kv[t] < 0 or the id is not in [0, vocab).
+void embed(int dtype, float* x, const void* E, int vocab, const int32_t* tokens, const int32_t* slot_kv,
+           int T, int d, hipStream_t s);
+
+// out[t] = x[t] / sqrt(mean(x[t]^2) + eps) * g, stored in dtype.
+void rmsnorm(int dtype, const float* x, const float* g, void* out, int T, int d, float eps, hipStream_t s);
+
+// hidden[slot_kv[t]] = RMSNorm(x[t]) * g (float32) for every slot with slot_kv[t] >= 0.
+void rmsnorm_unpack(const float* x, const float* g, float* hidden, const int32_t* slot_kv, int T, int d,
+                    float eps, hipStream_t s);
+
+// Rotate-half RoPE, in place, on the first n_heads_rot heads of every row of qkv (row
+// stride ld elements) at position slot_pos[t]; rows with slot_seg[t] < 0 are skipped.
+void rope_apply(int dtype, void* qkv, int64_t ld, const float2* table, const int32_t* slot_pos,
+                const int32_t* slot_seg, int T, int n_heads_rot, int D, hipStream_t s);
+
+// kc[slot_kv[t]] = qkv[t][k_col : k_col+kvw], vc[slot_kv[t]] = qkv[t][k_col+kvw : k_col+2kvw].
+void kv_scatter(int dtype, const void* qkv, int64_t ld, int k_col, int kvw, void* kc, void* vc,
+                const int32_t* slot_kv, int T, hipStream_t s);
+
+// act[t][f] = SiLU(gu[t][g(f)]) * gu[t][g(f) + 16], g(f) = 32 (f / 16) + f % 16 (float32 path).
+void swiglu_f32(const float* gu, float* act, int T, int F, hipStream_t s);
+
+// Epilogues of the projection GEMMs C = A B^T (A [M, K] activations, B [N, K] weights).
+enum Epilogue { kStore = 0, kResidual = 1, kSwiGLU = 2 };
+
+// bf16 MFMA GEMM.  kStore: C bf16 [M, ldc]; kResidual: C float32 [M, ldc] += A B^T;
+// kSwiGLU: B rows interleaved in blocks of 16 (gate, up) and C bf16 [M, ldc] holds
+// SiLU(gate) * up.  M-tiles whose slots all lie outside every span are skipped when
+// slot_seg is non-null.  Requires N % 256 == 0 and K % 64 == 0.
+void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+               int M, int N, int K, const int32_t* slot_seg, int capacity, hipStream_t s);
+
+// float32 FMA GEMM (kStore / kResidual).  Requires K % 16 == 0.
+void gemm_f32(int epi, const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
+              int M, int N, int K, hipStream_t s);
+
+// Attention over segments (independent mask): for every query slot of every work-list
+// tile, softmax(q k^T / sqrt(D)) v over the keys of its own segment at or before it.
+// qkv rows hold [Q (H heads) | K (Hkv heads) | V (Hkv heads)], D = 128.
+void attention_bf16(const void* qkv, int64_t ld, void* out, int64_t ldo, const int32_t* seg_start,
+                    const int32_t* seg_len, const int32_t* qtile_seg, const int32_t* qtile_q0,
+                    int n_qtiles, int H, int Hkv, int D, hipStream_t s);
+
+// float32 attention, one wavefront per (slot, head); slots outside every span are skipped.
+void attention_f32(const float* qkv, int64_t ld, float* out, int64_t ldo, const int32_t* slot_seg,
+                   const int32_t* seg_start, int T, int H, int Hkv, int D, hipStream_t s);
+
+}  // namespace ppk

@@ -1,0 +1,347 @@
+"""Python binding of the C ABI in ``include/prepack.h`` (ctypes).
+
+Argument marshalling only: every step of the packed prefill runs in the HIP
+library.  PyTorch provides device memory and streams.  The functions keep the
+C names: ``pp_pack``, ``pp_pack_padded``, ``pp_plan_bounds``,
+``pp_prefill_workspace_size``, ``pp_prefill``, ``pp_last_error``,
+``pp_version``.  A missing library raises ``LibraryMissing``; there is no
+fallback of any kind.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libprepack.so")
+
+PP_OK, PP_ERR_INVALID_ARG, PP_ERR_TOO_LONG, PP_ERR_BUFFER_TOO_SMALL, PP_ERR_UNSUPPORTED, PP_ERR_HIP = 0, -1, -2, -3, -4, -5
+PP_F32, PP_BF16 = 0, 1
+PP_EPI_STORE, PP_EPI_RESIDUAL, PP_EPI_SWIGLU = 0, 1, 2
+PP_QTILE = 128
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+class LibraryMissing(ImportError):
+    pass
+
+
+class PrepackError(RuntimeError):
+    def __init__(self, code: int, where: str, message: str):
+        super().__init__(f"{where} failed with status {code}: {message}")
+        self.code = code
+
+
+class PPPlan(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("n_rows", ctypes.c_int32),
+                ("max_len", ctypes.c_int32), ("total_len", ctypes.c_int32), ("n_qtiles", ctypes.c_int32),
+                ("slot_cap", ctypes.c_int64), ("qtile_cap", ctypes.c_int64),
+                ("row_seg_ptr", _i32p), ("seg_prompt", _i32p), ("seg_start", _i32p), ("seg_len", _i32p),
+                ("prompt_kv_off", _i32p), ("slot_seg", _i32p), ("slot_pos", _i32p), ("slot_kv", _i32p),
+                ("qtile_seg", _i32p), ("qtile_q0", _i32p)]
+
+
+class PPConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("dtype", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_theta", ctypes.c_float)]
+
+
+class PPWeights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
+                ("attn_norm", ctypes.POINTER(ctypes.c_void_p)), ("wqkv", ctypes.POINTER(ctypes.c_void_p)),
+                ("wo", ctypes.POINTER(ctypes.c_void_p)), ("mlp_norm", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_gateup", ctypes.POINTER(ctypes.c_void_p)), ("w_down", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class PPDPlan(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("n_rows", ctypes.c_int32),
+                ("max_len", ctypes.c_int32), ("total_len", ctypes.c_int32), ("n_qtiles", ctypes.c_int32),
+                ("seg_start", ctypes.c_void_p), ("seg_len", ctypes.c_void_p), ("slot_seg", ctypes.c_void_p),
+                ("slot_pos", ctypes.c_void_p), ("slot_kv", ctypes.c_void_p), ("qtile_seg", ctypes.c_void_p),
+                ("qtile_q0", ctypes.c_void_p)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises LibraryMissing if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise LibraryMissing(f"{LIB_PATH} is missing: build it with `python -m paper_2404_09529_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.pp_last_error.restype = ctypes.c_char_p
+        L.pp_version.restype = ctypes.c_char_p
+        L.pp_plan_bounds.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+                                     ctypes.POINTER(ctypes.c_int64)]
+        L.pp_pack.argtypes = [_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(PPPlan)]
+        L.pp_pack_padded.argtypes = [_i32p, ctypes.c_int32, ctypes.POINTER(PPPlan)]
+        L.pp_prefill_workspace_size.argtypes = [ctypes.POINTER(PPConfig), ctypes.POINTER(PPDPlan),
+                                                ctypes.POINTER(ctypes.c_size_t)]
+        L.pp_prefill.argtypes = [ctypes.POINTER(PPConfig), ctypes.POINTER(PPWeights), ctypes.POINTER(PPDPlan),
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+        cfgp, dpp = ctypes.POINTER(PPConfig), ctypes.POINTER(PPDPlan)
+        L.pp_embed.argtypes = [i32, vp, i32, i32, vp, dpp, vp, vp]
+        L.pp_rmsnorm.argtypes = [i32, vp, vp, i32, i32, f32, vp, vp]
+        L.pp_gemm.argtypes = [i32, i32, vp, i64, vp, i64, vp, i64, i32, i32, i32, dpp, vp]
+        L.pp_rope.argtypes = [cfgp, dpp, vp, vp, vp]
+        L.pp_kv_scatter.argtypes = [cfgp, dpp, vp, vp, vp, vp]
+        L.pp_attention.argtypes = [cfgp, dpp, vp, vp, vp]
+        L.pp_final_norm_unpack.argtypes = [vp, vp, i32, f32, dpp, vp, vp]
+        for name in ("pp_plan_bounds", "pp_pack", "pp_pack_padded", "pp_prefill_workspace_size", "pp_prefill",
+                     "pp_embed", "pp_rmsnorm", "pp_gemm", "pp_rope", "pp_kv_scatter", "pp_attention",
+                     "pp_final_norm_unpack"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def pp_last_error() -> str:
+    return lib().pp_last_error().decode()
+
+
+def pp_version() -> str:
+    return lib().pp_version().decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != PP_OK:
+        raise PrepackError(status, where, pp_last_error())
+
+
+# ----------------------------------------------------------------------------- planning
+@dataclass
+class Plan:
+    k: int
+    capacity: int
+    n_rows: int
+    max_len: int
+    total_len: int
+    row_seg_ptr: np.ndarray
+    seg_prompt: np.ndarray
+    seg_start: np.ndarray
+    seg_len: np.ndarray
+    prompt_kv_off: np.ndarray
+    slot_seg: np.ndarray
+    slot_pos: np.ndarray
+    slot_kv: np.ndarray
+    qtile_seg: np.ndarray
+    qtile_q0: np.ndarray
+
+    @property
+    def n_slots(self) -> int:
+        return self.n_rows * self.capacity
+
+    @property
+    def n_qtiles(self) -> int:
+        return int(self.qtile_seg.size)
+
+
+def pp_plan_bounds(k: int, C: int):
+    s, q = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().pp_plan_bounds(k, C, ctypes.byref(s), ctypes.byref(q)), "pp_plan_bounds")
+    return s.value, q.value
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(_i32p)
+
+
+def _run_pack(lengths: Sequence[int], capacity: Optional[int], slot_cap=None, qtile_cap=None) -> Plan:
+    L = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    k = int(L.size)
+    m = int(L.max()) if k else 0
+    C = m if (capacity is None or capacity == 0) else int(capacity)
+    bs, bq = pp_plan_bounds(k, max(C, 0)) if C >= 0 else (0, 0)
+    bs = bs if slot_cap is None else slot_cap
+    bq = bq if qtile_cap is None else qtile_cap
+    arrs = {n: np.zeros(max(size, 1), dtype=np.int32) for n, size in
+            [("row_seg_ptr", k + 1), ("seg_prompt", k), ("seg_start", k), ("seg_len", k),
+             ("prompt_kv_off", k + 1), ("slot_seg", bs), ("slot_pos", bs), ("slot_kv", bs),
+             ("qtile_seg", bq), ("qtile_q0", bq)]}
+    p = PPPlan(slot_cap=bs, qtile_cap=bq, **{n: _ptr(a) for n, a in arrs.items()})
+    if capacity is None:
+        _check(lib().pp_pack_padded(_ptr(L) if k else None, k, ctypes.byref(p)), "pp_pack_padded")
+    else:
+        _check(lib().pp_pack(_ptr(L) if k else None, k, int(capacity), ctypes.byref(p)), "pp_pack")
+    T = p.n_rows * p.capacity
+    return Plan(k=p.k, capacity=p.capacity, n_rows=p.n_rows, max_len=p.max_len, total_len=p.total_len,
+                row_seg_ptr=arrs["row_seg_ptr"][: p.n_rows + 1].copy(), seg_prompt=arrs["seg_prompt"][:k].copy(),
+                seg_start=arrs["seg_start"][:k].copy(), seg_len=arrs["seg_len"][:k].copy(),
+                prompt_kv_off=arrs["prompt_kv_off"][: k + 1].copy(), slot_seg=arrs["slot_seg"][:T].copy(),
+                slot_pos=arrs["slot_pos"][:T].copy(), slot_kv=arrs["slot_kv"][:T].copy(),
+                qtile_seg=arrs["qtile_seg"][: p.n_qtiles].copy(), qtile_q0=arrs["qtile_q0"][: p.n_qtiles].copy())
+
+
+def pp_pack(lengths: Sequence[int], capacity: int = 0, **caps) -> Plan:
+    """First-fit-decreasing packing into rows of ``capacity`` slots (0 = max length)."""
+    return _run_pack(lengths, capacity, **caps)
+
+
+def pp_pack_padded(lengths: Sequence[int], **caps) -> Plan:
+    """Full-batching plan: one right-padded row of length max(lengths) per prompt."""
+    return _run_pack(lengths, None, **caps)
+
+
+# ----------------------------------------------------------------------------- device side
+def _torch():
+    import torch
+    return torch
+
+
+class DevicePlan:
+    """A plan's arrays in device memory plus the pp_dplan struct that points at them."""
+
+    def __init__(self, plan: Plan, device="cuda"):
+        torch = _torch()
+        self.plan = plan
+        self.tensors = {n: torch.from_numpy(np.ascontiguousarray(getattr(plan, n))).to(device)
+                        for n in ("seg_start", "seg_len", "slot_seg", "slot_pos", "slot_kv", "qtile_seg", "qtile_q0")}
+        self.struct = PPDPlan(k=plan.k, capacity=plan.capacity, n_rows=plan.n_rows, max_len=plan.max_len,
+                              total_len=plan.total_len, n_qtiles=plan.n_qtiles,
+                              **{n: t.data_ptr() for n, t in self.tensors.items()})
+
+
+def interleave_gate_up(wg, wu):
+    """[F, d] x2 -> [2F, d] with rows 32j..32j+15 = wg[16j..16j+15], 32j+16..32j+31 = wu[16j..]."""
+    F, d = wg.shape
+    assert F % 16 == 0
+    return _torch().stack([wg.reshape(F // 16, 16, d), wu.reshape(F // 16, 16, d)], dim=1).reshape(2 * F, d)
+
+
+class DeviceModel:
+    """Decoder weights on the device in the library's layout, plus pp_config / pp_weights."""
+
+    def __init__(self, shape, weights: Dict, device="cuda"):
+        torch = _torch()
+        self.shape = shape
+        dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+        self.dtype_code = PP_BF16 if shape.dtype == "bf16" else PP_F32
+        self.torch_dtype = dt
+
+        def dev(a, t=dt):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device=device).to(t)
+
+        self.embed = dev(weights["embed"])
+        self.final_norm = dev(weights["final_norm"], torch.float32)
+        self.layers: List[Dict] = []
+        for L in weights["layers"][: shape.n_layers]:
+            wqkv = dev(np.concatenate([L["wq"], L["wk"], L["wv"]], axis=0))
+            self.layers.append(dict(
+                attn_norm=dev(L["attn_norm"], torch.float32), wqkv=wqkv, wo=dev(L["wo"]),
+                mlp_norm=dev(L["mlp_norm"], torch.float32),
+                w_gateup=interleave_gate_up(dev(L["wg"]), dev(L["wu"])).contiguous(), w_down=dev(L["wd"])))
+        n = shape.n_layers
+        self._arrays = {key: (ctypes.c_void_p * n)(*[Ld[key].data_ptr() for Ld in self.layers])
+                        for key in ("attn_norm", "wqkv", "wo", "mlp_norm", "w_gateup", "w_down")}
+        vp = ctypes.POINTER(ctypes.c_void_p)
+        self.weights_struct = PPWeights(embed=self.embed.data_ptr(), final_norm=self.final_norm.data_ptr(),
+                                        **{k: ctypes.cast(a, vp) for k, a in self._arrays.items()})
+        self.config = PPConfig(n_layers=n, d_model=shape.d_model, n_heads=shape.n_heads,
+                               n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn_dim=shape.ffn_dim,
+                               vocab=shape.vocab, dtype=self.dtype_code, rms_eps=shape.rms_eps,
+                               rope_theta=shape.rope_theta)
+
+
+def pp_prefill_workspace_size(model: DeviceModel, dplan: DevicePlan) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().pp_prefill_workspace_size(ctypes.byref(model.config), ctypes.byref(dplan.struct),
+                                           ctypes.byref(n)), "pp_prefill_workspace_size")
+    return n.value
+
+
+def pp_prefill(model: DeviceModel, dplan: DevicePlan, tokens, workspace, hidden, k_cache, v_cache,
+               stream=None) -> None:
+    """Enqueue the packed prefill on ``stream`` (default: torch's current stream)."""
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    _check(lib().pp_prefill(ctypes.byref(model.config), ctypes.byref(model.weights_struct),
+                            ctypes.byref(dplan.struct), tokens.data_ptr(), workspace.data_ptr(),
+                            workspace.numel() * workspace.element_size(), hidden.data_ptr(),
+                            k_cache.data_ptr(), v_cache.data_ptr(), ctypes.c_void_p(stream.cuda_stream)),
+           "pp_prefill")
+
+
+class Prefill:
+    """Outputs and workspace for one (model, plan) pair, allocated once with torch."""
+
+    def __init__(self, model: DeviceModel, dplan: DevicePlan, device="cuda"):
+        torch = _torch()
+        s = model.shape
+        L = dplan.plan.total_len
+        self.model, self.dplan = model, dplan
+        self.workspace = torch.empty(max(pp_prefill_workspace_size(model, dplan), 1), dtype=torch.uint8,
+                                     device=device)
+        self.hidden = torch.empty((L, s.d_model), dtype=torch.float32, device=device)
+        kv = (s.n_layers, L, s.n_kv_heads * s.head_dim)
+        self.k_cache = torch.empty(kv, dtype=model.torch_dtype, device=device)
+        self.v_cache = torch.empty(kv, dtype=model.torch_dtype, device=device)
+
+    def __call__(self, tokens, stream=None):
+        pp_prefill(self.model, self.dplan, tokens, self.workspace, self.hidden, self.k_cache, self.v_cache, stream)
+        return self.hidden, self.k_cache, self.v_cache
+
+
+# ----------------------------------------------------------------------------- single steps
+def config_of(shape, n_layers: Optional[int] = None) -> PPConfig:
+    return PPConfig(n_layers=shape.n_layers if n_layers is None else n_layers, d_model=shape.d_model,
+                    n_heads=shape.n_heads, n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim,
+                    ffn_dim=shape.ffn_dim, vocab=shape.vocab,
+                    dtype=PP_BF16 if shape.dtype == "bf16" else PP_F32, rms_eps=shape.rms_eps,
+                    rope_theta=shape.rope_theta)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = _torch().cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _p(t):
+    return None if t is None else t.data_ptr()
+
+
+def pp_embed(dtype: int, embed, vocab: int, d: int, tokens, dplan: DevicePlan, x, stream=None) -> None:
+    _check(lib().pp_embed(dtype, _p(embed), vocab, d, _p(tokens), ctypes.byref(dplan.struct), _p(x),
+                          _stream(stream)), "pp_embed")
+
+
+def pp_rmsnorm(dtype: int, x, gain, rows: int, d: int, eps: float, out, stream=None) -> None:
+    _check(lib().pp_rmsnorm(dtype, _p(x), _p(gain), rows, d, eps, _p(out), _stream(stream)), "pp_rmsnorm")
+
+
+def pp_gemm(dtype: int, epilogue: int, A, lda: int, B, ldb: int, C, ldc: int, M: int, N: int, K: int,
+            dplan: Optional[DevicePlan] = None, stream=None) -> None:
+    _check(lib().pp_gemm(dtype, epilogue, _p(A), lda, _p(B), ldb, _p(C), ldc, M, N, K,
+                         None if dplan is None else ctypes.byref(dplan.struct), _stream(stream)), "pp_gemm")
+
+
+def pp_rope(cfg: PPConfig, dplan: DevicePlan, qkv, table, stream=None) -> None:
+    _check(lib().pp_rope(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(qkv), _p(table), _stream(stream)),
+           "pp_rope")
+
+
+def pp_kv_scatter(cfg: PPConfig, dplan: DevicePlan, qkv, k_cache, v_cache, stream=None) -> None:
+    _check(lib().pp_kv_scatter(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(qkv), _p(k_cache), _p(v_cache),
+                               _stream(stream)), "pp_kv_scatter")
+
+
+def pp_attention(cfg: PPConfig, dplan: DevicePlan, qkv, out, stream=None) -> None:
+    _check(lib().pp_attention(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(qkv), _p(out), _stream(stream)),
+           "pp_attention")
+
+
+def pp_final_norm_unpack(x, gain, d: int, eps: float, dplan: DevicePlan, hidden, stream=None) -> None:
+    _check(lib().pp_final_norm_unpack(_p(x), _p(gain), d, eps, ctypes.byref(dplan.struct), _p(hidden),
+                                      _stream(stream)), "pp_final_norm_unpack")

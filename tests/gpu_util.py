@@ -1,0 +1,72 @@
+"""Helpers for the GPU parity tests: device transfers, bf16 ulps, error summaries.
+
+Expected values always come from ``oracle/`` run on the same seeded inputs; nothing
+here computes a result of the method.
+"""
+import numpy as np
+import torch
+
+from oracle import decoder as D
+from paper_2404_09529_amd import prepack as pp
+
+DEV = "cuda"
+
+
+def require_gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    pp.lib()  # raises LibraryMissing when the HIP library has not been built
+
+
+def bf16_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV).to(torch.bfloat16)
+
+
+def f32_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+def i32_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(DEV)
+
+
+def host64(t):
+    torch.cuda.synchronize()
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def rand_bf16(rng, shape, scale=1.0):
+    """Normal values already rounded to bf16 (float32 storage), so both sides see the same numbers."""
+    return D.round_bf16(rng.standard_normal(shape).astype(np.float32) * np.float32(scale))
+
+
+def bf16_ulp(x):
+    """Spacing of bf16 numbers at |x| (8 significant bits)."""
+    a = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), np.finfo(np.float32).tiny)
+    return np.exp2(np.floor(np.log2(a)) - 7)
+
+
+def within_ulps(got, ref, n_ulps=1.0, atol=0.0):
+    """|got - round_bf16(ref)| <= n_ulps * ulp(ref) + atol, elementwise; returns the worst ratio."""
+    err = np.abs(got - D.round_bf16(ref))
+    bound = n_ulps * bf16_ulp(ref) + atol
+    return float(np.max(err / bound)) if err.size else 0.0
+
+
+def report(name, got, ref):
+    mx, mean = D.errors(got, ref)
+    print(f"[parity] {name}: max |err| {mx:.3e}  mean |err| {mean:.3e}", flush=True)
+    return mx, mean
+
+
+def gpu_prefill(case, plan, stream=None):
+    """Run pp_prefill through the C ABI; returns (hidden, [K_l], [V_l]) as float64 numpy."""
+    model = pp.DeviceModel(case.shape, case.weights)
+    dplan = pp.DevicePlan(plan)
+    run = pp.Prefill(model, dplan)
+    tokens = i32_dev(case.tokens)
+    run(tokens, stream)
+    torch.cuda.synchronize()
+    h = host64(run.hidden)
+    k = host64(run.k_cache)
+    v = host64(run.v_cache)
+    return h, [k[l] for l in range(case.shape.n_layers)], [v[l] for l in range(case.shape.n_layers)]

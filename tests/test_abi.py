@@ -1,0 +1,201 @@
+"""The C ABI on the CPU: the library loads, exports every declared entry point, packs
+bit-exactly like the oracle, and rejects bad arguments before enqueuing anything.
+No GPU work is launched here."""
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import ffd
+from paper_2404_09529_amd import prepack as pp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FIELDS = ("row_seg_ptr", "seg_prompt", "seg_start", "seg_len", "prompt_kv_off", "slot_seg", "slot_pos",
+          "slot_kv", "qtile_seg", "qtile_q0")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(pp.LIB_PATH):
+        pytest.fail("libprepack.so is not built (python -m paper_2404_09529_amd.build)")
+    return pp.lib()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "prepack.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pp_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert {"pp_pack", "pp_pack_padded", "pp_prefill", "pp_prefill_workspace_size"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_struct_layouts_match_header():
+    assert ctypes.sizeof(pp.PPPlan) == 6 * 4 + 2 * 8 + 10 * 8
+    assert ctypes.sizeof(pp.PPConfig) == 10 * 4
+    assert ctypes.sizeof(pp.PPDPlan) == 6 * 4 + 7 * 8
+    assert ctypes.sizeof(pp.PPWeights) == 8 * 8
+
+
+def test_version(L):
+    assert "gfx950" in pp.pp_version()
+
+
+def _same(plan, ref):
+    for s in ("k", "capacity", "n_rows", "max_len", "total_len"):
+        assert getattr(plan, s) == getattr(ref, s), s
+    for f in FIELDS:
+        assert np.array_equal(getattr(plan, f), getattr(ref, f)), f
+
+
+def test_golden_examples(L, golden_dir):
+    with open(os.path.join(golden_dir, "ffd_examples.json")) as f:
+        for ex in json.load(f)["examples"]:
+            p = pp.pp_pack(ex["lengths"], ex["capacity"])
+            assert p.seg_start.tolist() == ex["seg_start"]
+            assert p.slot_kv.tolist() == ex["slot_kv"]
+            assert p.slot_pos.tolist() == ex["slot_pos"]
+            assert p.prompt_kv_off.tolist() == ex["prompt_kv_off"]
+            bins = [p.seg_prompt[p.row_seg_ptr[r]:p.row_seg_ptr[r + 1]].tolist() for r in range(p.n_rows)]
+            assert bins == ex["bins"]
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.lists(st.integers(1, 300), min_size=1, max_size=60), st.integers(0, 200), st.booleans())
+def test_pack_bit_exact_vs_oracle(L, lengths, extra, default_capacity):
+    C = 0 if default_capacity else max(lengths) + extra
+    _same(pp.pp_pack(lengths, C), ffd.pack(lengths, C))
+
+
+@settings(max_examples=100, deadline=None)
+@given(st.lists(st.integers(1, 200), min_size=1, max_size=40))
+def test_pack_padded_bit_exact_vs_oracle(L, lengths):
+    _same(pp.pp_pack_padded(lengths), ffd.pack_padded(lengths))
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_pack_bit_exact_on_workload_lengths(L, wid):
+    from paper_2404_09529_amd import workloads as W
+    wl = W.workload(wid)
+    for seed in range(3):
+        lengths = W.draw_lengths(wl, seed)
+        _same(pp.pp_pack(lengths, wl.capacity), ffd.pack(lengths, wl.capacity))
+        assert pp.pp_pack(lengths, wl.capacity).n_rows == ffd.pack(lengths, wl.capacity).n_rows
+
+
+def test_empty_batch(L):
+    p = pp.pp_pack([], 64)
+    assert p.n_rows == 0 and p.total_len == 0 and p.n_qtiles == 0
+    p = pp.pp_pack_padded([])
+    assert p.n_rows == 0
+
+
+def test_errors(L):
+    with pytest.raises(pp.PrepackError) as e:
+        pp.pp_pack([3, 0, 2], 8)
+    assert e.value.code == pp.PP_ERR_INVALID_ARG and "length 0" in pp.pp_last_error()
+    with pytest.raises(pp.PrepackError) as e:
+        pp.pp_pack([3, -1], 8)
+    assert e.value.code == pp.PP_ERR_INVALID_ARG
+    with pytest.raises(pp.PrepackError) as e:
+        pp.pp_pack([3, 9, 2], 8)
+    assert e.value.code == pp.PP_ERR_TOO_LONG
+    with pytest.raises(pp.PrepackError) as e:
+        pp.pp_pack([3, 2], -4)
+    assert e.value.code == pp.PP_ERR_INVALID_ARG
+    with pytest.raises(pp.PrepackError) as e:
+        pp.pp_pack([3, 2, 4], 8, slot_cap=23)
+    assert e.value.code == pp.PP_ERR_BUFFER_TOO_SMALL
+    with pytest.raises(pp.PrepackError) as e:
+        pp.pp_pack_padded([3, 2, 4], qtile_cap=2)
+    assert e.value.code == pp.PP_ERR_BUFFER_TOO_SMALL
+    # a successful call clears the message
+    pp.pp_pack([1], 4)
+    assert pp.pp_last_error() == ""
+    # NULL plan
+    lengths = (ctypes.c_int32 * 2)(3, 4)
+    assert pp.lib().pp_pack(lengths, 2, 8, None) == pp.PP_ERR_INVALID_ARG
+    assert pp.lib().pp_plan_bounds(-1, 4, None, None) == pp.PP_ERR_INVALID_ARG
+
+
+def _cfg(**kw):
+    base = dict(n_layers=1, d_model=4096, n_heads=32, n_kv_heads=8, head_dim=128, ffn_dim=14336, vocab=1000,
+                dtype=pp.PP_BF16, rms_eps=1e-5, rope_theta=5e5)
+    base.update(kw)
+    return pp.PPConfig(**base)
+
+
+def _dplan(**kw):
+    base = dict(k=2, capacity=256, n_rows=2, max_len=200, total_len=300, n_qtiles=3,
+                **{n: 0x1000 for n in ("seg_start", "seg_len", "slot_seg", "slot_pos", "slot_kv", "qtile_seg",
+                                       "qtile_q0")})
+    base.update(kw)
+    return pp.PPDPlan(**base)
+
+
+def _ws(cfg, dp):
+    n = ctypes.c_size_t()
+    st_ = pp.lib().pp_prefill_workspace_size(ctypes.byref(cfg), ctypes.byref(dp), ctypes.byref(n))
+    return st_, n.value
+
+
+def test_workspace_size_and_config_validation(L):
+    st_, n = _ws(_cfg(), _dplan())
+    assert st_ == pp.PP_OK
+    T = 512
+    want = T * 4096 * 4 + T * 4096 * 2 + T * 6144 * 2 + T * 4096 * 2 + T * 14336 * 2 + 200 * 64 * 8
+    assert want <= n <= want + 8 * 256
+    assert _ws(_cfg(head_dim=96), _dplan())[0] == pp.PP_ERR_UNSUPPORTED
+    assert _ws(_cfg(n_kv_heads=5), _dplan())[0] == pp.PP_ERR_UNSUPPORTED
+    assert _ws(_cfg(head_dim=64, n_heads=64, n_kv_heads=16), _dplan())[0] == pp.PP_ERR_UNSUPPORTED  # bf16 needs D=128
+    assert _ws(_cfg(d_model=1000), _dplan())[0] == pp.PP_ERR_UNSUPPORTED
+    assert _ws(_cfg(ffn_dim=5500), _dplan())[0] == pp.PP_ERR_UNSUPPORTED
+    assert _ws(_cfg(dtype=7), _dplan())[0] == pp.PP_ERR_INVALID_ARG
+    assert _ws(_cfg(n_layers=0), _dplan())[0] == pp.PP_ERR_INVALID_ARG
+    assert _ws(_cfg(dtype=pp.PP_F32, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=688),
+               _dplan())[0] == pp.PP_OK
+    assert _ws(_cfg(), _dplan(total_len=600))[0] == pp.PP_ERR_INVALID_ARG        # more tokens than slots (512)
+    assert _ws(_cfg(), _dplan(max_len=300))[0] == pp.PP_ERR_INVALID_ARG          # longer than a row
+    assert _ws(_cfg(), _dplan(slot_kv=0))[0] == pp.PP_ERR_INVALID_ARG            # NULL device array
+
+
+def _weights(n_layers):
+    arr = (ctypes.c_void_p * n_layers)(*([0x2000] * n_layers))
+    vp = ctypes.POINTER(ctypes.c_void_p)
+    w = pp.PPWeights(embed=0x2000, final_norm=0x2000,
+                     **{k: ctypes.cast(arr, vp) for k in ("attn_norm", "wqkv", "wo", "mlp_norm", "w_gateup",
+                                                          "w_down")})
+    return w, arr
+
+
+def test_prefill_rejects_before_enqueue(L):
+    """Every check of pp_prefill runs on the host before a launch, so these never touch a GPU."""
+    cfg, dp = _cfg(), _dplan()
+    w, keep = _weights(1)
+    f = pp.lib().pp_prefill
+    _, need = _ws(cfg, dp)
+    args = lambda ws, nbytes, hid=0x3000: (ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(dp), 0x4000, ws,
+                                           nbytes, hid, 0x5000, 0x6000, None)
+    assert f(*args(0x10000, need - 1)) == pp.PP_ERR_BUFFER_TOO_SMALL
+    assert f(*args(0x10000 + 8, need)) == pp.PP_ERR_INVALID_ARG        # misaligned workspace
+    assert f(*args(None, need)) == pp.PP_ERR_INVALID_ARG
+    assert f(*args(0x10000, need, hid=None)) == pp.PP_ERR_INVALID_ARG
+    assert f(ctypes.byref(cfg), None, ctypes.byref(dp), 0x4000, 0x10000, need, 0x3000, 0x5000, 0x6000,
+             None) == pp.PP_ERR_INVALID_ARG
+    bad = (ctypes.c_void_p * 1)(None)
+    w.wo = ctypes.cast(bad, ctypes.POINTER(ctypes.c_void_p))
+    assert f(*args(0x10000, need)) == pp.PP_ERR_INVALID_ARG
+    assert "layer 0" in pp.pp_last_error()
+    # an empty plan is a no-op that succeeds without touching any pointer
+    empty = _dplan(k=0, n_rows=0, capacity=0, max_len=0, total_len=0, n_qtiles=0)
+    w2, keep2 = _weights(1)
+    assert f(ctypes.byref(cfg), ctypes.byref(w2), ctypes.byref(empty), None, None, 0, None, None, None,
+             None) == pp.PP_OK

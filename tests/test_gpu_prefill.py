@@ -1,0 +1,160 @@
+"""End-to-end parity of pp_prefill on the GPU against the oracle.
+
+* float32 model (the tiny workload): the stated bar, max |err| <= 2e-2 and mean |err| <= 2e-3
+  on final hidden states and every layer's K/V, against the float64 oracle.
+* bf16 models at their real layer shapes: a bf16 pipeline cannot meet that absolute bar
+  end to end (bf16 storage alone moves a K/V value of magnitude 4..8 by up to 0.016, and
+  rounding noise compounds through the layers), so the GPU's error against the float64
+  oracle is gated against the error of an ideal bf16 pipeline: the same oracle with every
+  stored value rounded to bf16 (``oracle.decoder`` with ``rnd=round_bf16``).  Gate: mean
+  error <= 1.5x and max error <= 2x that floor.  The absolute-bar figures are printed.
+* packed and padded prefill on the GPU give bit-identical caches and hidden states for the
+  real tokens (the paper's exactness claim, section 3.3), since every row's arithmetic is
+  the same in both layouts.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as D
+from paper_2404_09529_amd import prepack as pp
+from paper_2404_09529_amd import workloads as W
+
+from .gpu_util import gpu_prefill, report, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+BAR_MAX, BAR_MEAN = 2e-2, 2e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _oracle(case, rnd=None, prompts=None):
+    kw = {} if rnd is None else {"rnd": rnd}
+    return D.prefill_per_prompt(case.lengths, case.tokens, case.weights, D.Shape.of(case.shape),
+                                prompts=prompts, **kw)
+
+
+def _rows(case, prompts):
+    off = np.concatenate([[0], np.cumsum(case.lengths)])
+    return np.concatenate([np.arange(off[i], off[i + 1]) for i in prompts])
+
+
+def _check_bar(name, gpu, ref, n_layers, rows=slice(None)):
+    h, k, v = gpu
+    out = [report(f"{name} hidden", h[rows], ref.hidden[rows])]
+    for l in range(n_layers):
+        out.append(report(f"{name} K{l}", k[l][rows], ref.k[l][rows]))
+        out.append(report(f"{name} V{l}", v[l][rows], ref.v[l][rows]))
+    return out
+
+
+# ----------------------------------------------------------------------------- float32: the stated bar
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("padded", [False, True])
+def test_tiny_fp32_workload_meets_bar(seed, padded):
+    case = W.make_case(1, seed, random_gains=True)
+    plan = pp.pp_pack_padded(case.lengths) if padded else pp.pp_pack(case.lengths, case.capacity)
+    gpu = gpu_prefill(case, plan)
+    ref = _oracle(case)
+    for mx, mean in _check_bar(f"tiny seed{seed} padded={padded}", gpu, ref, case.shape.n_layers):
+        assert mx <= BAR_MAX and mean <= BAR_MEAN
+
+
+def test_tiny_fp32_deeper_model():
+    case = W.make_case(1, 3, n_layers=3, random_gains=True, k=12)
+    gpu = gpu_prefill(case, pp.pp_pack(case.lengths, case.capacity))
+    for mx, mean in _check_bar("tiny 3 layers", gpu, _oracle(case), 3):
+        assert mx <= BAR_MAX and mean <= BAR_MEAN
+
+
+# ----------------------------------------------------------------------------- bf16 layer shapes
+def _gate(name, gpu_errs, floor_errs):
+    for (gm, ga), (fm, fa) in zip(gpu_errs, floor_errs):
+        assert ga <= 1.5 * fa + 1e-4, f"{name}: mean {ga:.3e} vs bf16 floor {fa:.3e}"
+        assert gm <= 2.0 * fm + 1e-3, f"{name}: max {gm:.3e} vs bf16 floor {fm:.3e}"
+    worst = max(e[0] for e in gpu_errs), max(e[1] for e in gpu_errs)
+    print(f"[parity] {name}: absolute bar (2e-2 / 2e-3) {'met' if worst[0] <= BAR_MAX and worst[1] <= BAR_MEAN else 'not met'}"
+          f" (worst max {worst[0]:.3e}, worst mean {worst[1]:.3e})", flush=True)
+
+
+BF16_CASES = [
+    # workload, layers, lengths, capacity
+    (2, 1, [1, 37, 128, 129, 300, 611], 1024),      # Llama-2-7B shape
+    (4, 1, [90, 257, 8, 700], 1024),                # Llama-3-8B shape, GQA 32/8, theta 5e5
+    (5, 2, [32, 480, 33, 1000], 1536),              # 1.3B shape
+]
+
+
+@pytest.mark.parametrize("wid,n_layers,lengths,cap", BF16_CASES)
+def test_bf16_layer_shapes_vs_oracle(wid, n_layers, lengths, cap):
+    case = W.make_case(wid, 0, n_layers=n_layers, lengths=lengths, random_gains=True)
+    gpu = gpu_prefill(case, pp.pp_pack(lengths, cap))
+    name = f"{case.wl.name} L{n_layers}"
+    errs = _check_bar(name, gpu, _oracle(case), n_layers)
+    floor = _check_bar(name + " bf16-floor", _floor(case), _oracle(case), n_layers)
+    _gate(name, errs, floor)
+
+
+def _floor(case, prompts=None):
+    r = _oracle(case, rnd=D.round_bf16, prompts=prompts)
+    return r.hidden, r.k, r.v
+
+
+# ----------------------------------------------------------------------------- packed == padded (section 3.3)
+@pytest.mark.parametrize("wid,n_layers,lengths,cap", [(2, 1, [5, 300, 129, 64, 1], 512), (1, 1, [4, 60, 33], 128)])
+def test_packed_equals_padded_bit_exact(wid, n_layers, lengths, cap):
+    case = W.make_case(wid, 1, n_layers=n_layers, lengths=lengths, random_gains=True)
+    a = gpu_prefill(case, pp.pp_pack(lengths, cap))
+    b = gpu_prefill(case, pp.pp_pack_padded(lengths))
+    assert np.array_equal(a[0], b[0])
+    for l in range(n_layers):
+        assert np.array_equal(a[1][l], b[1][l])
+        assert np.array_equal(a[2][l], b[2][l])
+
+
+# ----------------------------------------------------------------------------- edge cases
+@pytest.mark.parametrize("lengths,cap", [
+    ([1], 256),                  # one token
+    ([256], 256),                # a prompt filling its row exactly
+    ([1] * 70, 64),              # many one-token prompts, several rows
+    ([200, 100, 56, 3], 1000),   # row length not a multiple of the GEMM tile
+    ([129, 129, 129], 300),      # every row ends in padding that straddles a tile
+])
+def test_bf16_edge_cases(lengths, cap):
+    case = W.make_case(2, 2, n_layers=1, lengths=lengths, random_gains=True)
+    gpu = gpu_prefill(case, pp.pp_pack(lengths, cap))
+    name = f"edge {lengths[:4]} C{cap}"
+    _gate(name, _check_bar(name, gpu, _oracle(case), 1), _check_bar(name + " floor", _floor(case), _oracle(case), 1))
+
+
+def test_empty_batch_is_a_noop():
+    case = W.make_case(2, 0, n_layers=1, lengths=[5], random_gains=False)
+    model = pp.DeviceModel(case.shape, case.weights)
+    dplan = pp.DevicePlan(pp.pp_pack([], 4096))
+    out = torch.empty(0, device="cuda")
+    pp.pp_prefill(model, dplan, out, out, out, out, out)
+    torch.cuda.synchronize()
+
+
+# ----------------------------------------------------------------------------- full size, sampled
+def test_full_size_7b_lognormal_sampled_prompts():
+    """The benchmark's own workload and launch configuration (64 prompts, 4 layers, rows of
+    4096); the oracle recomputes three prompts from scratch (the shortest, a median one and
+    the longest that stays cheap) and the GPU's rows for them are compared."""
+    case = W.make_case(2, 0)
+    plan = pp.pp_pack(case.lengths, case.capacity)
+    gpu = gpu_prefill(case, plan)
+    order = np.argsort(case.lengths)
+    picks = [int(order[0]), int(order[len(order) // 2]), int(order[-12])]
+    print(f"[parity] full-size sampled prompts {picks} lengths {case.lengths[picks].tolist()}", flush=True)
+    rows = _rows(case, picks)
+    ref = _oracle(case, prompts=picks)
+    floor = _floor(case, prompts=picks)
+    name = "7B lognormal full size"
+    _gate(name, _check_bar(name, gpu, ref, 4, rows), _check_bar(name + " floor", floor, ref, 4, rows))
+    # every real token of every prompt was written, and nothing is non-finite
+    assert np.all(np.isfinite(gpu[0]))
