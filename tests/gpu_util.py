@@ -70,3 +70,23 @@ def gpu_prefill(case, plan, stream=None):
     k = host64(run.k_cache)
     v = host64(run.v_cache)
     return h, [k[l] for l in range(case.shape.n_layers)], [v[l] for l in range(case.shape.n_layers)]
+
+
+def check_bar(name, got, ref, bar_max=2e-2, bar_mean=2e-3, stored_bf16=True):
+    """The absolute bar (max / mean |err|) wherever the output format allows it.
+
+    For bf16-stored outputs the floor is the error of the correctly rounded exact result,
+    round_bf16(ref) - ref.  Where that floor already exceeds the bar (outputs of large
+    magnitude), the GPU must stay within 10% of the floor instead."""
+    mx, mean = report(name, got, ref)
+    if not stored_bf16:
+        assert mx <= bar_max and mean <= bar_mean, name
+        return mx, mean
+    fmx, fmean = D.errors(D.round_bf16(ref), ref)
+    lim_max = bar_max if fmx <= bar_max else 1.1 * fmx
+    lim_mean = bar_mean if fmean <= bar_mean else 1.1 * fmean
+    if (lim_max, lim_mean) != (bar_max, bar_mean):
+        print(f"[parity] {name}: bf16 rounding floor {fmx:.3e} / {fmean:.3e} exceeds the bar; "
+              f"gated at 1.1x the floor", flush=True)
+    assert mx <= lim_max and mean <= lim_mean, (name, mx, mean, lim_max, lim_mean)
+    return mx, mean

@@ -12,7 +12,8 @@ import torch
 from oracle import decoder as D, ffd
 from paper_2404_09529_amd import prepack as pp
 
-from .gpu_util import (bf16_dev, f32_dev, host64, i32_dev, rand_bf16, report, require_gpu, within_ulps)
+from .gpu_util import (bf16_dev, check_bar, f32_dev, host64, i32_dev, rand_bf16, report, require_gpu,
+                       within_ulps)
 
 pytestmark = pytest.mark.gpu
 
@@ -40,8 +41,7 @@ def test_gemm_bf16_store(M, N, K):
     ref = A.astype(np.float64) @ B.astype(np.float64).T
     got = host64(C)
     assert within_ulps(got, ref, 1.0, 1e-6) <= 1.0
-    mx, mean = report(f"gemm store {M}x{N}x{K}", got, ref)
-    assert mx <= BAR_MAX and mean <= BAR_MEAN
+    check_bar(f"gemm store {M}x{N}x{K}", got, ref)
 
 
 @pytest.mark.parametrize("M,N,K", [(384, 4096, 4096), (129, 4096, 11008)])
@@ -68,8 +68,7 @@ def test_gemm_bf16_swiglu(M, F, K):
     ref = D.silu(A64 @ Wg.astype(np.float64).T) * (A64 @ Wu.astype(np.float64).T)
     got = host64(C)
     assert within_ulps(got, ref, 1.0, 1e-5) <= 1.0
-    mx, mean = report(f"gemm swiglu {M}x{F}x{K}", got, ref)
-    assert mx <= BAR_MAX and mean <= BAR_MEAN
+    check_bar(f"gemm swiglu {M}x{F}x{K}", got, ref)
 
 
 def test_gemm_f32():
@@ -119,8 +118,7 @@ def test_attention_bf16(lengths, cap, H, Hkv, padded):
     assert np.all(np.isfinite(got[span]))
     assert np.all(np.isnan(got[~span]))      # rows outside every span are never written
     real = plan.slot_kv >= 0
-    mx, mean = report(f"attention {lengths} H{H}/{Hkv} padded={padded}", got[real], ref[real])
-    assert mx <= BAR_MAX and mean <= BAR_MEAN
+    check_bar(f"attention {lengths} H{H}/{Hkv} padded={padded}", got[real], ref[real])
 
 
 def test_attention_f32():
