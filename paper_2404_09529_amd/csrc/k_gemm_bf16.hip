@@ -4,24 +4,23 @@
 // C[M, N] = A[M, K] B[N, K]^T with A the packed activations (bf16, K contiguous) and B a
 // weight matrix in [out, in] layout (bf16, K contiguous), float32 accumulation.
 //
-// Tiling: one 256-thread workgroup (4 wavefronts) per 256 x 256 output tile, K consumed in
-// steps of 64.  Each wavefront owns a 128 (N) x 128 (M) sub-tile = 4 x 4 blocks of the
-// 32x32x16 bf16 MFMA, 256 accumulator registers.  The weight block is the MFMA's first
+// Tiling: one 512-thread workgroup (8 wavefronts) per 256 x 256 output tile, K consumed in
+// steps of 64.  Each wavefront owns a 128 (N) x 64 (M) sub-tile = 4 x 2 blocks of the
+// 32x32x16 bf16 MFMA, 128 accumulator registers.  The weight block is the MFMA's first
 // operand, so a lane's accumulators are 4-element runs along N of one activation row:
 // the epilogue writes 8-byte (bf16) or 16-byte (float32) runs without a transpose.
 //
-// Data path per K step: global -> registers (16-byte loads, 8 threads per 128-byte row)
-// for step k+1 while the matrix cores consume step k from LDS; LDS is double-buffered
-// (2 x 64 KB) so one barrier per step suffices.  LDS rows are 128 bytes = 8 chunks of 16
-// bytes; chunk c of row r is stored at c ^ f(r), f(r) = (r ^ r>>3) & 7, which makes the
-// fragment reads (32 rows x one chunk per half-wavefront) hit distinct banks whether the
-// LDS serves 8 or 16 lanes of a 16-byte read per cycle.
+// Data path: tiles go straight from global memory into LDS (buffer loads with the LDS
+// destination, no staging registers), double-buffered (2 x 64 KB).  Eight wavefronts, two
+// per SIMD, run a ping-pong schedule: while one wavefront of a SIMD reads a whole K step of
+// MFMA fragments from LDS, the other issues its 32 MFMAs back to back, and they swap at
+// every barrier.
 //
 // Scheduling: a launch has far more tiles than the 256 CUs.  Workgroups are dealt to the
 // 8 XCDs round-robin, so the linear workgroup id is remapped to make each XCD's
-// workgroups a contiguous range of tiles, and tiles are ordered in groups of 8 M-tiles
+// workgroups a contiguous range of tiles, and tiles are ordered in groups of 4 M-tiles
 // sweeping N, so the tiles resident on one XCD share activation and weight panels in its
-// L2.  M-tiles made only of row-tail padding are skipped (packed batches only carry pads
+// L2 (measured ~80% L2 hits on the 7B shapes).  M-tiles made only of row-tail padding are skipped (packed batches only carry pads
 // at row tails, section 3.1).
 #include "device.h"
 #include "kernels.h"
@@ -29,16 +28,21 @@
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int NT = 256;
-constexpr int CH = BK * 2 / 16;  // 16-byte chunks per LDS row
-constexpr int GROUP_M = 8;
+constexpr int NT = 512;                 // 8 wavefronts, 2 per SIMD
+constexpr int GROUP_M = 4;
+constexpr int ROW_B = BK * 2;           // LDS row: 128 bytes = 8 chunks of 16 bytes
+constexpr int OP_B = BM * ROW_B;        // one operand tile in LDS (32 KB)
+constexpr int STAGE_B = 2 * OP_B;       // A tile then B tile (64 KB); two stages = 128 KB
+constexpr int LOADS = BM * ROW_B / 1024 / 4;  // 1 KB direct-to-LDS loads per wavefront per stage (8)
+// Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
+constexpr int kRsrcWord3 = 0x00020000;
 
-struct Stage {
-    u32x4 a[BM * CH];
-    u32x4 b[BN * CH];
-};
+// LDS swizzle: logical 16-byte chunk c of tile row r is stored at chunk c ^ f(r).  With
+// f(r) = (r ^ r>>3) & 7, the 32 rows x one chunk read by a half-wavefront for an MFMA
+// fragment hit distinct banks whether the LDS serves 8 or 16 lanes per cycle.
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
 
-__device__ __forceinline__ int swz(int row, int c) { return c ^ ((row ^ (row >> 3)) & 7); }
+typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ bool tile_active(const int32_t* slot_seg, int capacity, int m0, int M) {
     if (!slot_seg || slot_seg[m0] >= 0) return true;
@@ -47,8 +51,11 @@ __device__ __forceinline__ bool tile_active(const int32_t* slot_seg, int capacit
     return next_row < min(m0 + BM, M);
 }
 
-template <typename V>
-__device__ __forceinline__ bf16x8 as_bf16x8(V v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ void barrier() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
 
 template <int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ A, int64_t lda,
@@ -56,8 +63,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
                                                        void* __restrict__ Cv, int64_t ldc, int M, int K,
                                                        const int32_t* __restrict__ slot_seg, int capacity,
                                                        int tiles_m, int tiles_n) {
-    __shared__ Stage st[2];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
 
     // ---- which tile: XCD-contiguous remap of the workgroup id, then grouped order
     const int total = tiles_m * tiles_n;
@@ -74,79 +82,120 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
     const int m0 = mt * BM, n0 = nt * BN;
     if (!tile_active(slot_seg, capacity, m0, M)) return;
 
-    // ---- global staging: thread owns chunk lc of rows lrow + 32 i, i < 8
-    const int lrow = tid >> 3, lc = tid & 7;
-    const bf16* a_src[8];
-    bool a_ok[8];
+    // ---- direct global -> LDS loads.  A stage holds the A tile then the B tile, 8 chunks of
+    // 16 bytes per row.  Load t of wavefront w fills 1 KB = rows 8 j .. 8 j + 7 of its operand
+    // (j = (w % 4) * 8 + t; wavefronts 0-3 load A, 4-7 load B); lane l lands at physical chunk
+    // l % 8 of row 8 j + l / 8, so it fetches the logical chunk that the swizzle puts there.
+    // Every quad of lanes reads one aligned 64-byte half of a row.  Rows of A past M read as
+    // zero (the descriptor ends at row min(M, m0 + 256)); every access is inside its buffer.
+    const int a_rows = min(M - m0, BM);
+    const bool load_b = wave >= 4;
+    const __amdgpu_buffer_rsrc_t rsrc = load_b
+        ? __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(B + int64_t(n0) * ldb), 0,
+                                            static_cast<int>(BN * ldb * 2), kRsrcWord3)
+        : __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A + int64_t(m0) * lda), 0,
+                                            static_cast<int>(a_rows * lda * 2), kRsrcWord3);
+    const int64_t ld = load_b ? ldb : lda;
+    int voff[LOADS];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int m = m0 + lrow + 32 * i;
-        a_ok[i] = m < M;
-        a_src[i] = A + int64_t(a_ok[i] ? m : m0) * lda + lc * 8;
+    for (int t = 0; t < LOADS; ++t) {
+        const int row = 8 * ((wave & 3) * LOADS + t) + lane / 8;
+        voff[t] = static_cast<int>(row * ld * 2) + 16 * ((lane & 7) ^ swz(row));
     }
-    const bf16* b_src = B + int64_t(n0 + lrow) * ldb + lc * 8;
-    const int64_t b_step = 32 * ldb;
-    u32x4 ra[8], rb[8];
-
-    auto gload = [&](int k0) {
+    const int lds_op = load_b ? OP_B : 0;
+    auto issue_loads = [&](int kt) {
+        char* stage = smem + (kt & 1) * STAGE_B + lds_op;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            ra[i] = a_ok[i] ? *reinterpret_cast<const u32x4*>(a_src[i] + k0) : u32x4{0u, 0u, 0u, 0u};
-            rb[i] = *reinterpret_cast<const u32x4*>(b_src + i * b_step + k0);
-        }
-    };
-    auto sstore = [&](Stage& s) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int r = lrow + 32 * i;
-            s.a[r * CH + swz(r, lc)] = ra[i];
-            s.b[r * CH + swz(r, lc)] = rb[i];
+        for (int t = 0; t < LOADS; ++t) {
+            lds_void* dst = (lds_void*)(stage + ((wave & 3) * LOADS + t) * 1024);   // generic -> LDS
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[t], kt * BK * 2, 0, 0);
         }
     };
 
-    f32x16 acc[4][4];
+    // ---- wavefront sub-tile: 128 (N) x 64 (M) = 4 x 2 MFMA blocks of 32 x 32
+    const int wn = wave & 1, wm = wave >> 1;
+    const int grp = wave >> 2;               // waves w and w + 4 share a SIMD
+    const int fr = lane & 31, fh = lane >> 5;
+    f32x16 acc[4][2];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-    const int wn = wave >> 1, wm = wave & 1;
-    const int fr = lane & 31, fh = lane >> 5;
-    const int nk = K / BK;
-
-    gload(0);
-    sstore(st[0]);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const Stage& cur = st[kt & 1];
-        if (kt + 1 < nk) gload((kt + 1) * BK);
+    // fragment addresses.  Row r = base + 32 i + fr of either operand has swizzle
+    // f(r) = g ^ 4 (i & 1) with g = ((fr & 7) ^ (fr >> 3)) & 7 (base is a multiple of 64), so
+    // the physical chunk of logical chunk 2 ks + fh is (2 (ks ^ 2 (i & 1))) ^ (fh ^ g): four
+    // per-lane offsets cover every (ks, i); the block stride (32 rows = 4 KB) is immediate.
+    const int gsw = ((fr & 7) ^ (fr >> 3)) & 7;
+    const int x = fh ^ gsw;
+    int a_lds[4], b_lds[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        a_lds[m] = (wm * 64 + fr) * ROW_B + 16 * ((2 * m) ^ x);
+        b_lds[m] = OP_B + (wn * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
+    }
+    bf16x8 fw[BK / 16][4], fa[BK / 16][2];
+    auto read_frags = [&](int kt) {
+        const char* stage = smem + (kt & 1) * STAGE_B;
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
-            bf16x8 bw[4], ba[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = wn * 128 + i * 32 + fr;
-                bw[i] = as_bf16x8(cur.b[r * CH + swz(r, ks * 2 + fh)]);
-            }
+            for (int i = 0; i < 4; ++i)
+                fw[ks][i] = *reinterpret_cast<const bf16x8*>(stage + b_lds[ks ^ (2 * (i & 1))] + i * 32 * ROW_B);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int r = wm * 128 + j * 32 + fr;
-                ba[j] = as_bf16x8(cur.a[r * CH + swz(r, ks * 2 + fh)]);
-            }
+            for (int j = 0; j < 2; ++j)
+                fa[ks][j] = *reinterpret_cast<const bf16x8*>(stage + a_lds[ks ^ (2 * (j & 1))] + j * 32 * ROW_B);
+        }
+    };
+    auto mfmas = [&]() {
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[i], ba[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[ks][i], fa[ks][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+    };
+
+    // ---- ping-pong over K.  Group 0 runs [memory, MFMA] phases; group 1 runs the same one
+    // phase later, so on every SIMD one wavefront issues MFMAs while the other reads LDS.
+    // Tile kt+1 is requested in phase 2kt by both groups and waited for at the end of
+    // phase 2kt+1, so every load has two phases to land; a stage is refilled only after
+    // both groups have read it.  Both groups execute 2 nk + 2 barriers.
+    const int nk = K / BK;
+    issue_loads(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    barrier();
+    if (grp == 0) {
+        for (int kt = 0; kt < nk; ++kt) {
+            if (kt + 1 < nk) issue_loads(kt + 1);
+            read_frags(kt);
+            __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
+            barrier();
+            mfmas();
+            __builtin_amdgcn_s_waitcnt(0x0f70);          // vmcnt(0): this group's part of tile kt+1
+            barrier();
         }
-        if (kt + 1 < nk) sstore(st[(kt + 1) & 1]);
-        __syncthreads();
+        barrier();
+    } else {
+        if (nk > 1) issue_loads(1);
+        barrier();
+        for (int kt = 0; kt < nk; ++kt) {
+            read_frags(kt);
+            __builtin_amdgcn_s_waitcnt(0);               // fragments, and this group's part of tile kt+1
+            barrier();
+            if (kt + 2 < nk) issue_loads(kt + 2);
+            mfmas();
+            barrier();
+        }
     }
 
     // ---- epilogue: lane holds, for activation row m, runs of 4 consecutive n
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int m = m0 + wm * 128 + j * 32 + fr;
+    for (int j = 0; j < 2; ++j) {
+        const int m = m0 + wm * 64 + j * 32 + fr;
         if (m >= M) continue;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -197,17 +246,28 @@ void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, 
     const dim3 grid(tiles_m * tiles_n);
     const bf16* a = static_cast<const bf16*>(A);
     const bf16* b = static_cast<const bf16*>(B);
+    constexpr size_t lds = 2 * STAGE_B;
+    static bool attr = [] {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<kStore>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<kResidual>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<kSwiGLU>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        return true;
+    }();
+    (void)attr;
     switch (epi) {
         case kStore:
-            gemm_bf16_kernel<kStore><<<grid, NT, 0, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
+            gemm_bf16_kernel<kStore><<<grid, NT, lds, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
                                                          tiles_m, tiles_n);
             break;
         case kResidual:
-            gemm_bf16_kernel<kResidual><<<grid, NT, 0, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
+            gemm_bf16_kernel<kResidual><<<grid, NT, lds, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
                                                             tiles_m, tiles_n);
             break;
         default:
-            gemm_bf16_kernel<kSwiGLU><<<grid, NT, 0, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
+            gemm_bf16_kernel<kSwiGLU><<<grid, NT, lds, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
                                                           tiles_m, tiles_n);
             break;
     }
