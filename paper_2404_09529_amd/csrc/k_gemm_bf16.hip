@@ -29,7 +29,6 @@ namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int NT = 512;                 // 8 wavefronts, 2 per SIMD
-constexpr int GROUP_M = 4;
 constexpr int ROW_B = BK * 2;           // LDS row: 128 bytes = 8 chunks of 16 bytes
 constexpr int OP_B = BM * ROW_B;        // one operand tile in LDS (32 KB)
 constexpr int STAGE_B = 2 * OP_B;       // A tile then B tile (64 KB); two stages = 128 KB
@@ -67,18 +66,23 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
 
-    // ---- which tile: XCD-contiguous remap of the workgroup id, then grouped order
-    const int total = tiles_m * tiles_n;
+    // ---- which tile.  Workgroups are dealt to the 8 XCDs round-robin (XCD = id % 8).  XCD x
+    // owns the contiguous block of M-tiles [x pm, x pm + pm) and walks it in groups of at
+    // most 8 M-tiles, each group sweeping all N-tiles.  Every XCD starts at N-tile 0 at the
+    // same time and advances at the same rate, so the weight panels are fetched from HBM
+    // once into the last-level cache and shared by all XCDs, while each XCD's activation
+    // panels stay resident; the ~32 tiles an XCD runs at once (about 8 M x 4 N) share
+    // panels in its L2.  Workgroups past an XCD's block exit at once.
     const int g = blockIdx.x;
     const int xcd = g & 7, local = g >> 3;
-    const int full = total >> 3, rem = total & 7;
-    const int lin = xcd < rem ? xcd * (full + 1) + local : rem * (full + 1) + (xcd - rem) * full + local;
-    const int group = lin / (GROUP_M * tiles_n);
-    const int first_m = group * GROUP_M;
-    const int gsz = min(tiles_m - first_m, GROUP_M);
-    const int in_group = lin - group * GROUP_M * tiles_n;
-    const int mt = first_m + in_group % gsz;
-    const int nt = in_group / gsz;
+    const int pm = (tiles_m + 7) / 8;
+    const int m_begin = xcd * pm, m_cnt = min(pm, tiles_m - m_begin);
+    if (m_cnt <= 0 || local >= m_cnt * tiles_n) return;
+    const int n_groups = (m_cnt + 7) / 8, gm = (m_cnt + n_groups - 1) / n_groups;
+    const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
+    const int first = group * gm, gsz = min(m_cnt - first, gm);
+    const int mt = m_begin + first + within % gsz;
+    const int nt = within / gsz;
     const int m0 = mt * BM, n0 = nt * BN;
     if (!tile_active(slot_seg, capacity, m0, M)) return;
 
@@ -161,17 +165,17 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
 
     // ---- ping-pong over K.  Group 0 runs [memory, MFMA] phases; group 1 runs the same one
     // phase later, so on every SIMD one wavefront issues MFMAs while the other reads LDS.
-    // Tile kt+1 is requested in phase 2kt by both groups and waited for at the end of
-    // phase 2kt+1, so every load has two phases to land; a stage is refilled only after
-    // both groups have read it.  Both groups execute 2 nk + 2 barriers.
+    // Tile kt+1 is requested in phase 2kt (group 0 in its memory phase, group 1 at the end
+    // of its MFMA phase) and waited for at the end of phase 2kt+1; a stage is refilled only
+    // after both groups have read it.  Both groups execute 2 nk + 2 barriers.
     const int nk = K / BK;
     issue_loads(0);
     __builtin_amdgcn_s_waitcnt(0);
     barrier();
     if (grp == 0) {
         for (int kt = 0; kt < nk; ++kt) {
-            if (kt + 1 < nk) issue_loads(kt + 1);
             read_frags(kt);
+            if (kt + 1 < nk) issue_loads(kt + 1);        // after the LDS reads: they start first
             __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
             barrier();
             mfmas();
@@ -186,8 +190,11 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
             read_frags(kt);
             __builtin_amdgcn_s_waitcnt(0);               // fragments, and this group's part of tile kt+1
             barrier();
-            if (kt + 2 < nk) issue_loads(kt + 2);
             mfmas();
+            // issued after the MFMA burst so the load issue does not delay it; tile kt+2 goes
+            // to the stage both groups finished reading in phases 2kt and 2kt+1, and is
+            // waited for at the end of this group's next memory phase (phase 2kt+3)
+            if (kt + 2 < nk) issue_loads(kt + 2);
             barrier();
         }
     }
@@ -243,7 +250,7 @@ void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, 
                int N, int K, const int32_t* slot_seg, int capacity, hipStream_t s) {
     if (M <= 0) return;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
-    const dim3 grid(tiles_m * tiles_n);
+    const dim3 grid(8 * ((tiles_m + 7) / 8) * tiles_n);   // XCD-blocked order; extras exit
     const bf16* a = static_cast<const bf16*>(A);
     const bf16* b = static_cast<const bf16*>(B);
     constexpr size_t lds = 2 * STAGE_B;
