@@ -3,22 +3,27 @@
 // each query tile its key range directly.
 //
 // bf16 kernel (head dim 128), one 256-thread workgroup per (query tile, head):
-//   * a work-list entry is (segment, q0): queries [q0, q0+128) of one segment, so keys
-//     [0, min(q0+128, len)) of the same segment are the only ones ever loaded -- every
-//     tile outside the prompt's diagonal block is skipped by construction, and only the
-//     last key tiles (the diagonal) need an in-tile causal predicate;
+//   * a work-list entry is (segment, q0): queries [q0, q0+128) of one segment, so only keys
+//     [0, min(q0+128, len)) of the same segment are ever used -- every tile outside the
+//     prompt's diagonal block of M' is skipped by construction;
+//   * key tiles of 64 start at the segment's first key, so only the diagonal tile and the
+//     span's tail need a predicate, and the arithmetic of a query is the same wherever its
+//     prompt sits (packed and padded layouts give identical results);
 //   * wavefront w owns queries q0 + 32w .. q0 + 32w + 31; its Q fragments stay in
 //     registers for the whole key loop;
-//   * key tiles of 64 are staged through LDS, double-buffered: K as [key][d] rows of 256
-//     bytes (chunk c of row r stored at c ^ (r & 15)), V transposed to [d][key] rows of
-//     128 bytes so that the value product contracts over keys with 16-byte fragment reads;
-//   * S^T = K Q^T and O^T += V^T P^T run on the 32x32x16 bf16 MFMA; a lane holds one
-//     query, so the running max / sum of the online softmax (Milakov and Gimelshein 2018;
-//     the tiling of FlashAttention, Dao et al. 2022) are lane-local plus one exchange with
-//     the lane 32 away; probabilities are fed back as bf16 in registers (the key order of
-//     the transposed V tile is permuted to match the accumulator layout of S^T);
-//   * query heads sharing a KV head (GQA) are adjacent workgroups, so their K/V tiles are
-//     read from L2.
+//   * K and V tiles go from global memory straight into LDS (16-byte direct-to-LDS loads,
+//     double-buffered), both row-major [key][d] with XOR-swizzled 16-byte chunks; the
+//     swizzle is applied on the global side of each load;
+//   * S^T = K Q^T and O^T += V^T P^T run on the 32x32x16 bf16 MFMA; a lane holds one query,
+//     so the running max / sum of the online softmax (Milakov and Gimelshein 2018; the
+//     tiling of FlashAttention, Dao et al. 2022) are lane-local plus one exchange with the
+//     lane 32 away;
+//   * the V operand of O^T += V^T P^T is read with the transposing LDS read
+//     (ds_read_b64_tr_b16), with key rows chosen so that its key order matches the order in
+//     which the S^T accumulators hold the probabilities: P feeds the MFMA from registers
+//     as is;
+//   * query heads sharing a KV head (GQA) are adjacent workgroups, so their K/V tiles come
+//     from L2.
 // float32 kernel: one wavefront per (query slot, head), a plain online-softmax loop over
 // the query's keys, used for float32 models.
 #include "device.h"
@@ -31,118 +36,120 @@ constexpr int BQ = PP_QTILE;  // queries per workgroup
 constexpr int BKV = 64;       // keys per tile
 constexpr int HD = 128;       // head dim of the bf16 kernel
 constexpr int NT = 256;
+constexpr int ROW = HD * 2;                  // LDS bytes per key row (16 chunks of 16 bytes)
+constexpr int TILE_B = BKV * ROW;            // one K or V tile: 16 KB
+constexpr int STAGE_B = 2 * TILE_B;          // K tile then V tile; two stages = 64 KB
+constexpr int LOADS = TILE_B / 1024 / 4;     // 1 KB loads per wavefront per tile (4)
+// Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
+constexpr int kRsrcWord3 = 0x00020000;
 
-struct KVTile {
-    u32x4 k[BKV * (HD / 8)];   // [64 keys][16 chunks]
-    u32x4 vt[HD * (BKV / 8)];  // [128 d][8 chunks]
-};
+typedef __attribute__((address_space(3))) void lds_void;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-__device__ __forceinline__ int kswz(int row, int c) { return c ^ (row & 15); }
-__device__ __forceinline__ int vswz(int row, int c) { return c ^ ((row ^ (row >> 3)) & 7); }
-// Position of key j (within a 64-key tile) in a row of the transposed V tile: bits 2 and 3
-// swapped, matching which keys a lane's probabilities cover in the S^T accumulator layout.
-__device__ __forceinline__ int vperm(int j) { return (j & ~12) | ((j >> 1) & 4) | ((j << 1) & 8); }
+// K rows: chunk c of key row r stored at c ^ (r & 15): the MFMA fragment reads (32 rows x
+// one chunk per half-wavefront) hit distinct banks.  V rows: chunk c stored at c ^ vswz(r),
+// vswz = 0, 4, 10, 14 for r & 3 = 0..3: the transposing reads (4 consecutive rows x 32 or 64
+// bytes per 16 or 32 lanes) hit distinct banks whether the LDS serves 8 or 16 lanes of a
+// 16-byte access per cycle.
+__device__ __forceinline__ int kswz(int r) { return r & 15; }
+__device__ __forceinline__ int vswz(int r) { return (0xEA40 >> (4 * (r & 3))) & 15; }
 
 template <typename V>
 __device__ __forceinline__ bf16x8 as_bf16x8(V v) { return __builtin_bit_cast(bf16x8, v); }
 
-__global__ __launch_bounds__(NT) void attn_bf16_kernel(const bf16* __restrict__ qkv, int64_t ld,
-                                                       bf16* __restrict__ out, int64_t ldo,
-                                                       const int32_t* __restrict__ seg_start,
-                                                       const int32_t* __restrict__ seg_len,
-                                                       const int32_t* __restrict__ qtile_seg,
-                                                       const int32_t* __restrict__ qtile_q0, int H, int Hkv,
-                                                       float scale_log2) {
-    __shared__ KVTile sm[2];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict__ qkv, int64_t ld,
+                                                          bf16* __restrict__ out, int64_t ldo,
+                                                          const int32_t* __restrict__ seg_start,
+                                                          const int32_t* __restrict__ seg_len,
+                                                          const int32_t* __restrict__ qtile_seg,
+                                                          const int32_t* __restrict__ qtile_q0, int H, int Hkv,
+                                                          float scale_log2) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int w = blockIdx.x / H, h = blockIdx.x - (blockIdx.x / H) * H;
     const int seg = qtile_seg[w], q0 = qtile_q0[w];
-    const int64_t a = seg_start[seg];
-    const int n = seg_len[seg];
+    const int a = seg_start[seg], n = seg_len[seg];
     const int g = h / (H / Hkv);
-    const int n_kv = min(q0 + BQ, n);  // keys [0, n_kv) of the segment
+    const int n_kv = min(q0 + BQ, n);                 // keys [0, n_kv) of the segment
     const int nkt = (n_kv + BKV - 1) / BKV;
 
-    const bf16* Qp = qkv + int64_t(h) * HD;
-    const bf16* Kp = qkv + int64_t(H + g) * HD;
-    const bf16* Vp = qkv + int64_t(H + Hkv + g) * HD;
-
     const int fr = lane & 31, fh = lane >> 5;
-    const int qi = q0 + wave * 32 + fr;  // this lane's query (offset in the segment)
+    const int qi = q0 + wave * 32 + fr;               // this lane's query (offset in the segment)
     const bool q_ok = qi < n;
     const int wq_lo = q0 + wave * 32;
     const int wq_hi = min(wq_lo + 31, n - 1);
 
     bf16x8 qf[HD / 16];
     {
-        const bf16* qrow = Qp + (a + (q_ok ? qi : 0)) * ld + fh * 8;
+        const bf16* qrow = qkv + int64_t(a + (q_ok ? qi : 0)) * ld + int64_t(h) * HD + fh * 8;
 #pragma unroll
         for (int ks = 0; ks < HD / 16; ++ks)
             qf[ks] = q_ok ? as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + ks * 16)) : bf16x8{};
     }
 
-    u32x4 rk[4], rv[4];
-    auto gload = [&](int kt) {
-        const int kb = kt * BKV;
+    // ---- direct-to-LDS loads.  The descriptor spans the segment's key rows [a, a + n_kv), so
+    // rows past the span read as zero; load t of wavefront w fills key rows 4 j .. 4 j + 3 of
+    // a tile (j = 4 w + t), lane l landing at physical chunk l % 16 of row 4 j + l / 16.
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>(qkv + int64_t(a) * ld), 0, static_cast<int>(n_kv * ld * 2), kRsrcWord3);
+    const int kcol = (H + g) * HD, vcol = (H + Hkv + g) * HD;
+    int koff[LOADS], voff[LOADS];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int key = kb + (tid >> 4) + 16 * i;
-            rk[i] = key < n_kv ? *reinterpret_cast<const u32x4*>(Kp + (a + key) * ld + (tid & 15) * 8)
-                               : u32x4{0u, 0u, 0u, 0u};
-        }
-        const int vkey = kb + (tid & 63);
+    for (int t = 0; t < LOADS; ++t) {
+        const int pr = 4 * (wave * LOADS + t) + lane / 16, pc = lane & 15;
+        koff[t] = static_cast<int>(pr * ld * 2) + (kcol + 8 * (pc ^ kswz(pr))) * 2;
+        voff[t] = static_cast<int>(pr * ld * 2) + (vcol + 8 * (pc ^ vswz(pr))) * 2;
+    }
+    auto issue = [&](int kt) {
+        char* stage = smem + (kt & 1) * STAGE_B;
+        const int soff = static_cast<int>(kt * BKV * ld * 2);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int dc = (tid >> 6) + 4 * i;
-            rv[i] = vkey < n_kv ? *reinterpret_cast<const u32x4*>(Vp + (a + vkey) * ld + dc * 8)
-                                : u32x4{0u, 0u, 0u, 0u};
-        }
-    };
-    auto sstore = [&](KVTile& t) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int row = (tid >> 4) + 16 * i;
-            t.k[row * 16 + kswz(row, tid & 15)] = rk[i];
-        }
-        const int pos = vperm(tid & 63);
-        const int pc = pos >> 3, pe = pos & 7;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int dc = (tid >> 6) + 4 * i;
-            const bf16x8 v = as_bf16x8(rv[i]);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int d = dc * 8 + e;
-                bf16* rowp = reinterpret_cast<bf16*>(&t.vt[d * 8]);
-                rowp[vswz(d, pc) * 8 + pe] = v[e];
-            }
+        for (int t = 0; t < LOADS; ++t) {
+            const int j = wave * LOADS + t;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(stage + j * 1024), 16, koff[t], soff, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(stage + TILE_B + j * 1024), 16, voff[t], soff,
+                                                     0, 0);
         }
     };
+
+    // ---- fragment addresses.  K: row b*32 + fr, chunk (2 ks + fh) ^ (fr & 15).  V (transposing
+    // read r of sub-step `sub`, d block db): this lane supplies the address of key row
+    // sub*16 + 8 r + 4 (grp / 2) + lane16 / 4 and d columns db*32 + 16 (grp % 2) + 4 (lane16 % 4)
+    // .. +3, where grp = lane / 16; the lane then receives 4 consecutive keys of one d.
+    const int k_lds = fr * ROW;
+    const int kx = fh ^ (fr & 15);                    // chunk (2 ks + fh) ^ (fr & 15) = 2 ks ^ kx
+    const int l16 = lane & 15, grp16 = lane >> 4;
+    const int vrow = 4 * (grp16 >> 1) + (l16 >> 2);   // + sub*16 + 8 r; vrow & 3 = l16 >> 2
+    const int vd = 16 * (grp16 & 1) + 4 * (l16 & 3);   // + db*32
+    const int vs = vswz(vrow);
 
     f32x16 o[HD / 32];
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db) o[db] = f32x16{};
     float m_i = -1e30f, l_i = 0.f;
 
-    gload(0);
-    sstore(sm[0]);
-    __syncthreads();
+    issue(0);
     for (int kt = 0; kt < nkt; ++kt) {
-        const KVTile& cur = sm[kt & 1];
-        if (kt + 1 < nkt) gload(kt + 1);
-        const int kb = kt * BKV;
+        __builtin_amdgcn_s_waitcnt(0x0f70);            // vmcnt(0): this wavefront's loads of tile kt
+        __builtin_amdgcn_s_barrier();                  // everyone's loads landed; stage of kt-1 free
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 1 < nkt) issue(kt + 1);
+        const char* stage = smem + (kt & 1) * STAGE_B;
+        const int kb = kt * BKV;                       // first key of the tile
         if (kb <= wq_hi) {
             f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
             for (int ks = 0; ks < HD / 16; ++ks) {
 #pragma unroll
                 for (int b = 0; b < 2; ++b) {
-                    const int row = b * 32 + fr;
-                    const bf16x8 kf = as_bf16x8(cur.k[row * 16 + kswz(row, ks * 2 + fh)]);
+                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(stage + k_lds + b * 32 * ROW +
+                                                                       16 * ((2 * ks) ^ kx));
                     s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[b], 0, 0, 0);
                 }
             }
-            const bool need_mask = (kb + BKV - 1 > wq_lo) || (kb + BKV > n_kv);
+            const bool need_mask = kb + BKV - 1 > wq_lo || kb + BKV > n_kv;
             float mx = -INFINITY;
 #pragma unroll
             for (int b = 0; b < 2; ++b)
@@ -180,19 +187,24 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(const bf16* __restrict__ 
                 for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(s[sub >> 1][(sub & 1) * 8 + e]);
 #pragma unroll
                 for (int db = 0; db < HD / 32; ++db) {
-                    const int row = db * 32 + fr;
-                    const bf16x8 vf = as_bf16x8(cur.vt[row * 8 + vswz(row, sub * 2 + fh)]);
+                    s16x4 v2[2];
+#pragma unroll
+                    for (int r = 0; r < 2; ++r) {
+                        const int row = sub * 16 + 8 * r + vrow;
+                        const int d = db * 32 + vd;
+                        const char* p = stage + TILE_B + row * ROW + 16 * ((d >> 3) ^ vs) + (d & 7) * 2;
+                        v2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));   // generic -> LDS
+                    }
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
                     o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[db], 0, 0, 0);
                 }
             }
         }
-        if (kt + 1 < nkt) sstore(sm[(kt + 1) & 1]);
-        __syncthreads();
     }
 
     if (!q_ok) return;
     const float inv_l = 1.0f / l_i;
-    bf16* orow = out + (a + qi) * ldo + int64_t(h) * HD + fh * 4;
+    bf16* orow = out + int64_t(a + qi) * ldo + int64_t(h) * HD + fh * 4;
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
@@ -255,10 +267,16 @@ void attention_bf16(const void* qkv, int64_t ld, void* out, int64_t ldo, const i
                     const int32_t* seg_len, const int32_t* qtile_seg, const int32_t* qtile_q0, int n_qtiles, int H,
                     int Hkv, int D, hipStream_t s) {
     if (n_qtiles <= 0) return;
+    static bool attr = [] {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bf16_kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, 2 * STAGE_B);
+        return true;
+    }();
+    (void)attr;
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
-    attn_bf16_kernel<<<dim3(n_qtiles * H), NT, 0, s>>>(static_cast<const bf16*>(qkv), ld, static_cast<bf16*>(out),
-                                                        ldo, seg_start, seg_len, qtile_seg, qtile_q0, H, Hkv,
-                                                        scale_log2);
+    attn_bf16_kernel<<<dim3(n_qtiles * H), NT, 2 * STAGE_B, s>>>(static_cast<const bf16*>(qkv), ld,
+                                                                 static_cast<bf16*>(out), ldo, seg_start, seg_len,
+                                                                 qtile_seg, qtile_q0, H, Hkv, scale_log2);
 }
 
 void attention_f32(const float* qkv, int64_t ld, float* out, int64_t ldo, const int32_t* slot_seg,

@@ -56,6 +56,15 @@ pp_status validate_config(const pp_config* c) {
     return PP_OK;
 }
 
+// The attention kernel addresses one segment's key rows through a 32-bit buffer range.
+pp_status validate_attention_span(const pp_config* c, const pp_dplan* p) {
+    const int64_t qkv_w = int64_t(c->n_heads + 2 * c->n_kv_heads) * c->head_dim;
+    if (c->dtype == PP_BF16 && (int64_t(p->max_len) + 2 * 64) * qkv_w * 2 > INT32_MAX)
+        return pp::fail(PP_ERR_UNSUPPORTED, "max_len %d too long for the attention kernel at this width",
+                        p->max_len);
+    return PP_OK;
+}
+
 pp_status validate_plan(const pp_dplan* p) {
     if (!p) return pp::fail(PP_ERR_INVALID_ARG, "plan is NULL");
     if (p->k < 0 || p->capacity < 0 || p->n_rows < 0 || p->max_len < 0 || p->total_len < 0 || p->n_qtiles < 0)
@@ -113,6 +122,7 @@ extern "C" pp_status pp_prefill_workspace_size(const pp_config* cfg, const pp_dp
     pp::clear_error();
     if (pp_status st = validate_config(cfg)) return st;
     if (pp_status st = validate_plan(plan)) return st;
+    if (pp_status st = validate_attention_span(cfg, plan)) return st;
     if (!bytes) return pp::fail(PP_ERR_INVALID_ARG, "bytes is NULL");
     *bytes = layout_of(cfg, plan).total;
     return PP_OK;
@@ -124,6 +134,7 @@ extern "C" pp_status pp_prefill(const pp_config* cfg, const pp_weights* w, const
     pp::clear_error();
     if (pp_status st = validate_config(cfg)) return st;
     if (pp_status st = validate_plan(plan)) return st;
+    if (pp_status st = validate_attention_span(cfg, plan)) return st;
     if (pp_status st = validate_weights(cfg, w)) return st;
     if (plan->total_len == 0) return PP_OK;
     if (!tokens || !hidden || !k_cache || !v_cache)
@@ -319,6 +330,7 @@ extern "C" pp_status pp_attention(const pp_config* cfg, const pp_dplan* plan, co
     pp::clear_error();
     if (pp_status st = validate_config(cfg)) return st;
     if (pp_status st = validate_plan(plan)) return st;
+    if (pp_status st = validate_attention_span(cfg, plan)) return st;
     const int T = plan->n_rows * plan->capacity;
     if (T == 0 || plan->total_len == 0) return PP_OK;
     if (!qkv || !out) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
