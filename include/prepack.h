@@ -166,8 +166,10 @@ typedef struct pp_weights {
  * n_rows * capacity entries, qtile arrays n_qtiles). */
 typedef struct pp_dplan {
     int32_t k, capacity, n_rows, max_len, total_len, n_qtiles;
+    const int32_t* seg_prompt;
     const int32_t* seg_start;
     const int32_t* seg_len;
+    const int32_t* prompt_kv_off;
     const int32_t* slot_seg;
     const int32_t* slot_pos;
     const int32_t* slot_kv;
@@ -239,6 +241,16 @@ pp_status pp_rmsnorm(int32_t dtype, const float* x, const float* gain, int32_t r
 pp_status pp_gemm(int32_t dtype, int32_t epilogue, const void* A, int64_t lda, const void* B, int64_t ldb,
                   void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, const pp_dplan* plan, void* stream);
 
+/* QKV projection with RESTART-PE and the KV-cache UNPACK fused into its epilogue (bf16 only;
+ * the float32 path uses pp_gemm + pp_rope + pp_kv_scatter): [q | k | v] = xn wqkv^T with
+ * float32 accumulation; q and k rotated (rotate-half RoPE) at each slot's restart position;
+ * q stored to q_out [n_rows*capacity, H D]; k and v stored straight into the layer's caches
+ * k_cache, v_cache [total_len, Hkv D] at row slot_kv[t] for every real slot t.
+ * xn [n_rows*capacity, d] bf16; wqkv [(H+2Hkv) D, d] bf16; table: device scratch of
+ * max_len * D/2 float2, filled by this call (cos/sin of position * theta^(-2i/D) in float64). */
+pp_status pp_qkv_projection(const pp_config* cfg, const pp_dplan* plan, const void* xn, const void* wqkv,
+                            void* table, void* q_out, void* k_cache, void* v_cache, void* stream);
+
 /* RESTART-PE (section 3.2): rotate-half RoPE in place on the query and key heads of
  * qkv [n_rows*capacity, (H+2Hkv)D] at each slot's restart position slot_pos; slots outside
  * every span are left alone.  table: device scratch of max_len * D/2 float2 (8 bytes each),
@@ -252,9 +264,13 @@ pp_status pp_kv_scatter(const pp_config* cfg, const pp_dplan* plan, const void* 
 
 /* Attention under the independent mask M' (section 3.2): for every slot of every segment,
  * softmax(q k^T / sqrt(D)) v over the keys of the same segment at or before it.
- * qkv [n_rows*capacity, (H+2Hkv)D] (post-RoPE), out [n_rows*capacity, H D], dtype; rows of
- * slots outside every span are not written. */
-pp_status pp_attention(const pp_config* cfg, const pp_dplan* plan, const void* qkv, void* out, void* stream);
+ * q: post-RoPE queries, row t at q + t * ldq (elements), H D per row, one row per slot;
+ * k_cache, v_cache: the layer's caches [total_len, Hkv D] (post-RoPE keys), keys of segment s
+ * at rows prompt_kv_off[seg_prompt[s]] + j; a key of a span that is no prompt token (full
+ * batching's padding) is read as zero.  out [n_rows*capacity, H D]; rows of slots outside
+ * every span are not written.  All in dtype. */
+pp_status pp_attention(const pp_config* cfg, const pp_dplan* plan, const void* q, int64_t ldq,
+                       const void* k_cache, const void* v_cache, void* out, void* stream);
 
 /* Final RMSNorm fused with the hidden-state UNPACK: hidden[slot_kv[t]] = RMSNorm(x[t]) * gain
  * for every real slot; x [n_rows*capacity, d] float32, hidden [total_len, d] float32. */

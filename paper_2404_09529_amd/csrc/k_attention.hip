@@ -11,9 +11,11 @@
 //     prompt sits (packed and padded layouts give identical results);
 //   * wavefront w owns queries q0 + 32w .. q0 + 32w + 31; its Q fragments stay in
 //     registers for the whole key loop;
-//   * K and V tiles go from global memory straight into LDS (16-byte direct-to-LDS loads,
-//     double-buffered), both row-major [key][d] with XOR-swizzled 16-byte chunks; the
-//     swizzle is applied on the global side of each load;
+//   * keys and values are read from the per-prompt caches that the QKV projection has just
+//     written (UNPACK happens before attention, so the packed layout never holds K or V):
+//     a segment's keys are contiguous cache rows.  K and V tiles go from there straight into
+//     LDS (16-byte direct-to-LDS loads, double-buffered), both row-major [key][d] with
+//     XOR-swizzled 16-byte chunks; the swizzle is applied on the global side of each load;
 //   * S^T = K Q^T and O^T += V^T P^T run on the 32x32x16 bf16 MFMA; a lane holds one query,
 //     so the running max / sum of the online softmax (Milakov and Gimelshein 2018; the
 //     tiling of FlashAttention, Dao et al. 2022) are lane-local plus one exchange with the
@@ -58,10 +60,13 @@ __device__ __forceinline__ int vswz(int r) { return (0xEA40 >> (4 * (r & 3))) & 
 template <typename V>
 __device__ __forceinline__ bf16x8 as_bf16x8(V v) { return __builtin_bit_cast(bf16x8, v); }
 
-__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict__ qkv, int64_t ld,
-                                                          bf16* __restrict__ out, int64_t ldo,
+__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict__ q, int64_t ldq,
+                                                          const bf16* __restrict__ kc, const bf16* __restrict__ vc,
+                                                          int64_t ldkv, bf16* __restrict__ out, int64_t ldo,
+                                                          const int32_t* __restrict__ seg_prompt,
                                                           const int32_t* __restrict__ seg_start,
                                                           const int32_t* __restrict__ seg_len,
+                                                          const int32_t* __restrict__ prompt_kv_off,
                                                           const int32_t* __restrict__ qtile_seg,
                                                           const int32_t* __restrict__ qtile_q0, int H, int Hkv,
                                                           float scale_log2) {
@@ -71,6 +76,8 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
     const int w = blockIdx.x / H, h = blockIdx.x - (blockIdx.x / H) * H;
     const int seg = qtile_seg[w], q0 = qtile_q0[w];
     const int a = seg_start[seg], n = seg_len[seg];
+    const int prompt = seg_prompt[seg];
+    const int kv0 = prompt_kv_off[prompt], plen = prompt_kv_off[prompt + 1] - kv0;
     const int g = h / (H / Hkv);
     const int n_kv = min(q0 + BQ, n);                 // keys [0, n_kv) of the segment
     const int nkt = (n_kv + BKV - 1) / BKV;
@@ -83,33 +90,41 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
 
     bf16x8 qf[HD / 16];
     {
-        const bf16* qrow = qkv + int64_t(a + (q_ok ? qi : 0)) * ld + int64_t(h) * HD + fh * 8;
+        const bf16* qrow = q + int64_t(a + (q_ok ? qi : 0)) * ldq + int64_t(h) * HD + fh * 8;
 #pragma unroll
         for (int ks = 0; ks < HD / 16; ++ks)
             qf[ks] = q_ok ? as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + ks * 16)) : bf16x8{};
     }
 
-    // ---- direct-to-LDS loads.  The descriptor spans the segment's key rows [a, a + n_kv), so
-    // rows past the span read as zero; load t of wavefront w fills key rows 4 j .. 4 j + 3 of
-    // a tile (j = 4 w + t), lane l landing at physical chunk l % 16 of row 4 j + l / 16.
-    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<bf16*>(qkv + int64_t(a) * ld), 0, static_cast<int>(n_kv * ld * 2), kRsrcWord3);
-    const int kcol = (H + g) * HD, vcol = (H + Hkv + g) * HD;
+    // ---- direct-to-LDS loads from the caches.  Key tile kt covers cache rows kv0 + 64 kt ..
+    // + 63; its descriptors start at that row and end at row kv0 + min(n_kv, plen), so rows
+    // past the prompt (a padded span's tail) and past the keys in use read as zero.  All
+    // offsets are in the per-lane part of the address, the part the range check covers.  Load
+    // t of wavefront w fills key rows 4 j .. 4 j + 3 of a tile (j = 4 w + t), lane l landing at
+    // physical chunk l % 16 of row 4 j + l / 16.
+    const int kv_rows = min(n_kv, plen);
+    const int row_b = static_cast<int>(ldkv) * 2;
+    const int col = g * HD;
     int koff[LOADS], voff[LOADS];
 #pragma unroll
     for (int t = 0; t < LOADS; ++t) {
         const int pr = 4 * (wave * LOADS + t) + lane / 16, pc = lane & 15;
-        koff[t] = static_cast<int>(pr * ld * 2) + (kcol + 8 * (pc ^ kswz(pr))) * 2;
-        voff[t] = static_cast<int>(pr * ld * 2) + (vcol + 8 * (pc ^ vswz(pr))) * 2;
+        koff[t] = pr * row_b + (col + 8 * (pc ^ kswz(pr))) * 2;
+        voff[t] = pr * row_b + (col + 8 * (pc ^ vswz(pr))) * 2;
     }
     auto issue = [&](int kt) {
         char* stage = smem + (kt & 1) * STAGE_B;
-        const int soff = static_cast<int>(kt * BKV * ld * 2);
+        const int64_t first = int64_t(kv0) + kt * BKV;
+        const int records = max(kv_rows - kt * BKV, 0) * row_b;
+        const __amdgpu_buffer_rsrc_t krsrc =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(kc + first * ldkv), 0, records, kRsrcWord3);
+        const __amdgpu_buffer_rsrc_t vrsrc =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(vc + first * ldkv), 0, records, kRsrcWord3);
 #pragma unroll
         for (int t = 0; t < LOADS; ++t) {
             const int j = wave * LOADS + t;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(stage + j * 1024), 16, koff[t], soff, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(stage + TILE_B + j * 1024), 16, voff[t], soff,
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, (lds_void*)(stage + j * 1024), 16, koff[t], 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(vrsrc, (lds_void*)(stage + TILE_B + j * 1024), 16, voff[t], 0,
                                                      0, 0);
         }
     };
@@ -217,10 +232,13 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
 }
 
 // ----------------------------------------------------------------------------- float32
-__global__ __launch_bounds__(NT) void attn_f32_kernel(const float* __restrict__ qkv, int64_t ld,
-                                                      float* __restrict__ out, int64_t ldo,
+__global__ __launch_bounds__(NT) void attn_f32_kernel(const float* __restrict__ q, int64_t ldq,
+                                                      const float* __restrict__ kc, const float* __restrict__ vc,
+                                                      int64_t ldkv, float* __restrict__ out, int64_t ldo,
                                                       const int32_t* __restrict__ slot_seg,
-                                                      const int32_t* __restrict__ seg_start, int T, int H,
+                                                      const int32_t* __restrict__ seg_prompt,
+                                                      const int32_t* __restrict__ seg_start,
+                                                      const int32_t* __restrict__ prompt_kv_off, int T, int H,
                                                       int Hkv, int D, float scale) {
     const int lane = threadIdx.x & 63;
     const int64_t wid = int64_t(blockIdx.x) * (NT / kWave) + (threadIdx.x >> 6);
@@ -229,20 +247,25 @@ __global__ __launch_bounds__(NT) void attn_f32_kernel(const float* __restrict__ 
     const int h = static_cast<int>(wid - slot * H);
     const int seg = slot_seg[slot];
     if (seg < 0) return;
-    const int64_t a = seg_start[seg];
+    const int qi = static_cast<int>(slot - seg_start[seg]);
+    const int prompt = seg_prompt[seg];
+    const int64_t kv0 = prompt_kv_off[prompt];
+    const int plen = prompt_kv_off[prompt + 1] - static_cast<int>(kv0);
     const int g = h / (H / Hkv);
-    const float* q = qkv + slot * ld + int64_t(h) * D;
+    const float* qr = q + slot * ldq + int64_t(h) * D;
     float qv[2], acc[2] = {0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < 2; ++c) qv[c] = lane + 64 * c < D ? q[lane + 64 * c] : 0.f;
+    for (int c = 0; c < 2; ++c) qv[c] = lane + 64 * c < D ? qr[lane + 64 * c] : 0.f;
     float m = -INFINITY, l = 0.f;
-    for (int64_t j = a; j <= slot; ++j) {
-        const float* k = qkv + j * ld + int64_t(H + g) * D;
-        const float* v = qkv + j * ld + int64_t(H + Hkv + g) * D;
+    for (int j = 0; j <= qi; ++j) {
+        // keys past the prompt (a padded span's tail) are zero: score 0, value 0
+        const bool real = j < plen;
+        const float* k = kc + (kv0 + j) * ldkv + int64_t(g) * D;
+        const float* v = vc + (kv0 + j) * ldkv + int64_t(g) * D;
         float part = 0.f;
 #pragma unroll
         for (int c = 0; c < 2; ++c)
-            if (lane + 64 * c < D) part += qv[c] * k[lane + 64 * c];
+            if (real && lane + 64 * c < D) part += qv[c] * k[lane + 64 * c];
         const float sc = wave_sum(part) * scale;
         const float m_new = fmaxf(m, sc);
         const float corr = expf(m - m_new);
@@ -250,7 +273,7 @@ __global__ __launch_bounds__(NT) void attn_f32_kernel(const float* __restrict__ 
         l = l * corr + p;
 #pragma unroll
         for (int c = 0; c < 2; ++c)
-            if (lane + 64 * c < D) acc[c] = acc[c] * corr + p * v[lane + 64 * c];
+            if (lane + 64 * c < D) acc[c] = acc[c] * corr + (real ? p * v[lane + 64 * c] : 0.f);
         m = m_new;
     }
     float* o = out + slot * ldo + int64_t(h) * D;
@@ -263,9 +286,10 @@ __global__ __launch_bounds__(NT) void attn_f32_kernel(const float* __restrict__ 
 
 namespace ppk {
 
-void attention_bf16(const void* qkv, int64_t ld, void* out, int64_t ldo, const int32_t* seg_start,
-                    const int32_t* seg_len, const int32_t* qtile_seg, const int32_t* qtile_q0, int n_qtiles, int H,
-                    int Hkv, int D, hipStream_t s) {
+void attention_bf16(const void* q, int64_t ldq, const void* kc, const void* vc, int64_t ldkv, void* out,
+                    int64_t ldo, const int32_t* seg_prompt, const int32_t* seg_start, const int32_t* seg_len,
+                    const int32_t* prompt_kv_off, const int32_t* qtile_seg, const int32_t* qtile_q0, int n_qtiles,
+                    int H, int Hkv, hipStream_t s) {
     if (n_qtiles <= 0) return;
     static bool attr = [] {
         (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bf16_kernel),
@@ -273,19 +297,21 @@ void attention_bf16(const void* qkv, int64_t ld, void* out, int64_t ldo, const i
         return true;
     }();
     (void)attr;
-    const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(D));
-    attn_bf16_kernel<<<dim3(n_qtiles * H), NT, 2 * STAGE_B, s>>>(static_cast<const bf16*>(qkv), ld,
-                                                                 static_cast<bf16*>(out), ldo, seg_start, seg_len,
-                                                                 qtile_seg, qtile_q0, H, Hkv, scale_log2);
+    const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(HD));
+    attn_bf16_kernel<<<dim3(n_qtiles * H), NT, 2 * STAGE_B, s>>>(
+        static_cast<const bf16*>(q), ldq, static_cast<const bf16*>(kc), static_cast<const bf16*>(vc), ldkv,
+        static_cast<bf16*>(out), ldo, seg_prompt, seg_start, seg_len, prompt_kv_off, qtile_seg, qtile_q0, H, Hkv,
+        scale_log2);
 }
 
-void attention_f32(const float* qkv, int64_t ld, float* out, int64_t ldo, const int32_t* slot_seg,
-                   const int32_t* seg_start, int T, int H, int Hkv, int D, hipStream_t s) {
+void attention_f32(const float* q, int64_t ldq, const float* kc, const float* vc, int64_t ldkv, float* out,
+                   int64_t ldo, const int32_t* slot_seg, const int32_t* seg_prompt, const int32_t* seg_start,
+                   const int32_t* prompt_kv_off, int T, int H, int Hkv, int D, hipStream_t s) {
     const int64_t waves = int64_t(T) * H;
     if (waves == 0) return;
     const unsigned blocks = static_cast<unsigned>((waves + NT / kWave - 1) / (NT / kWave));
-    attn_f32_kernel<<<blocks, NT, 0, s>>>(qkv, ld, out, ldo, slot_seg, seg_start, T, H, Hkv, D,
-                                          1.0f / sqrtf(static_cast<float>(D)));
+    attn_f32_kernel<<<blocks, NT, 0, s>>>(q, ldq, kc, vc, ldkv, out, ldo, slot_seg, seg_prompt, seg_start,
+                                          prompt_kv_off, T, H, Hkv, D, 1.0f / sqrtf(static_cast<float>(D)));
 }
 
 }  // namespace ppk

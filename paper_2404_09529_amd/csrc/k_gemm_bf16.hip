@@ -16,6 +16,11 @@
 // MFMA fragments from LDS, the other issues its 32 MFMAs back to back, and they swap at
 // every barrier.
 //
+// Epilogues: bf16 store; float32 residual add; SwiGLU over interleaved gate/up blocks; and,
+// for the QKV projection, RoPE at the restart positions (section 3.2) applied to the float32
+// accumulators, with queries stored to the packed batch and keys and values stored straight
+// into the per-prompt caches (the UNPACK of Algorithm 1).
+//
 // Scheduling: a launch has far more tiles than the 256 CUs.  Workgroups are dealt to the
 // 8 XCDs round-robin, so the linear workgroup id is remapped to make each XCD's
 // workgroups a contiguous range of tiles, and tiles are ordered in groups of 4 M-tiles
@@ -61,7 +66,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
                                                        const bf16* __restrict__ B, int64_t ldb,
                                                        void* __restrict__ Cv, int64_t ldc, int M, int K,
                                                        const int32_t* __restrict__ slot_seg, int capacity,
-                                                       int tiles_m, int tiles_n) {
+                                                       int tiles_m, int tiles_n, ppk::QkvOut qo) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
@@ -200,6 +205,60 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
     }
 
     // ---- epilogue: lane holds, for activation row m, runs of 4 consecutive n
+    if constexpr (EPI == ppk::kQkvRope) {
+        // The wavefront's 128 columns are exactly one head (tiles start at multiples of 256),
+        // and the rotate-half partners c and c + 64 are accumulator blocks i and i + 2 of the
+        // same lane: RoPE is applied to the float32 accumulators before the one rounding.
+        const int head = (n0 + wn * 128) >> 7;
+        const int kind = head < qo.H ? 0 : (head < qo.H + qo.Hkv ? 1 : 2);   // q, k, v (uniform)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int m = m0 + wm * 64 + j * 32 + fr;
+            if (m >= M) continue;
+            bf16* dst;
+            if (kind == 0) {
+                dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
+            } else {
+                const int kv = qo.slot_kv[m];
+                if (kv < 0) continue;
+                dst = static_cast<bf16*>(kind == 1 ? qo.kc : qo.vc) + int64_t(kv) * qo.ldkv +
+                      (head - qo.H - (kind == 2 ? qo.Hkv : 0)) * 128;
+            }
+            if (kind < 2) {
+                const int pos = slot_seg[m] >= 0 ? qo.slot_pos[m] : 0;
+                const float2* cs = qo.table + int64_t(pos) * 64 + fh * 4;
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const f32x4 t0 = *reinterpret_cast<const f32x4*>(cs + i * 32 + q * 8);
+                        const f32x4 t1 = *reinterpret_cast<const f32x4*>(cs + i * 32 + q * 8 + 2);
+                        const float cv[4] = {t0[0], t0[2], t1[0], t1[2]};
+                        const float sv[4] = {t0[1], t0[3], t1[1], t1[3]};
+                        bf16x4 lo, hi;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float a = acc[i][j][q * 4 + e], b = acc[i + 2][j][q * 4 + e];
+                            lo[e] = static_cast<bf16>(a * cv[e] - b * sv[e]);
+                            hi[e] = static_cast<bf16>(b * cv[e] + a * sv[e]);
+                        }
+                        *reinterpret_cast<bf16x4*>(dst + i * 32 + q * 8 + fh * 4) = lo;
+                        *reinterpret_cast<bf16x4*>(dst + 64 + i * 32 + q * 8 + fh * 4) = hi;
+                    }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        bf16x4 v;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(acc[i][j][q * 4 + e]);
+                        *reinterpret_cast<bf16x4*>(dst + i * 32 + q * 8 + fh * 4) = v;
+                    }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int m = m0 + wm * 64 + j * 32 + fr;
@@ -246,38 +305,42 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
 
 namespace ppk {
 
-void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc, int M,
-               int N, int K, const int32_t* slot_seg, int capacity, hipStream_t s) {
-    if (M <= 0) return;
-    const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
-    const dim3 grid(8 * ((tiles_m + 7) / 8) * tiles_n);   // XCD-blocked order; extras exit
-    const bf16* a = static_cast<const bf16*>(A);
-    const bf16* b = static_cast<const bf16*>(B);
-    constexpr size_t lds = 2 * STAGE_B;
+namespace {
+
+constexpr size_t kLds = 2 * STAGE_B;
+
+template <int EPI>
+void launch(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc, int M, int N, int K,
+            const int32_t* slot_seg, int capacity, const QkvOut& qo, hipStream_t s) {
     static bool attr = [] {
-        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<kStore>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<kResidual>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<kSwiGLU>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
         return true;
     }();
     (void)attr;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
+    const dim3 grid(8 * ((tiles_m + 7) / 8) * tiles_n);   // XCD-blocked order; extras exit
+    gemm_bf16_kernel<EPI><<<grid, NT, kLds, s>>>(static_cast<const bf16*>(A), lda, static_cast<const bf16*>(B),
+                                                ldb, C, ldc, M, K, slot_seg, capacity, tiles_m, tiles_n, qo);
+}
+
+}  // namespace
+
+void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc, int M,
+               int N, int K, const int32_t* slot_seg, int capacity, hipStream_t s) {
+    if (M <= 0) return;
+    const QkvOut none{};
     switch (epi) {
-        case kStore:
-            gemm_bf16_kernel<kStore><<<grid, NT, lds, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
-                                                         tiles_m, tiles_n);
-            break;
-        case kResidual:
-            gemm_bf16_kernel<kResidual><<<grid, NT, lds, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
-                                                            tiles_m, tiles_n);
-            break;
-        default:
-            gemm_bf16_kernel<kSwiGLU><<<grid, NT, lds, s>>>(a, lda, b, ldb, C, ldc, M, K, slot_seg, capacity,
-                                                          tiles_m, tiles_n);
-            break;
+        case kStore: launch<kStore>(A, lda, B, ldb, C, ldc, M, N, K, slot_seg, capacity, none, s); break;
+        case kResidual: launch<kResidual>(A, lda, B, ldb, C, ldc, M, N, K, slot_seg, capacity, none, s); break;
+        default: launch<kSwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, slot_seg, capacity, none, s); break;
     }
+}
+
+void qkv_rope_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, int M, int K, const int32_t* slot_seg,
+                   int capacity, const QkvOut& out, hipStream_t s) {
+    if (M <= 0) return;
+    launch<kQkvRope>(A, lda, B, ldb, nullptr, 0, M, (out.H + 2 * out.Hkv) * 128, K, slot_seg, capacity, out, s);
 }
 
 }  // namespace ppk

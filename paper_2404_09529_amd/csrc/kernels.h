@@ -34,7 +34,23 @@ void kv_scatter(int dtype, const void* qkv, int64_t ld, int k_col, int kvw, void
 void swiglu_f32(const float* gu, float* act, int T, int F, hipStream_t s);
 
 // Epilogues of the projection GEMMs C = A B^T (A [M, K] activations, B [N, K] weights).
-enum Epilogue { kStore = 0, kResidual = 1, kSwiGLU = 2 };
+enum Epilogue { kStore = 0, kResidual = 1, kSwiGLU = 2, kQkvRope = 3 };
+
+// Destinations of the kQkvRope epilogue.  B is the stacked [Wq; Wk; Wv] with head dim 128;
+// q [M, ldq] receives the rotated queries, kc / vc [*, ldkv] the rotated keys and the values
+// of every slot with slot_kv >= 0 at row slot_kv.  Rotation angles come from table
+// (float2 [positions][64]) at slot_pos; slots with slot_seg < 0 use position 0.
+struct QkvOut {
+    void* q;
+    int64_t ldq;
+    void* kc;
+    void* vc;
+    int64_t ldkv;
+    const float2* table;
+    const int32_t* slot_pos;
+    const int32_t* slot_kv;
+    int H, Hkv;
+};
 
 // bf16 MFMA GEMM.  kStore: C bf16 [M, ldc]; kResidual: C float32 [M, ldc] += A B^T;
 // kSwiGLU: B rows interleaved in blocks of 16 (gate, up) and C bf16 [M, ldc] holds
@@ -43,19 +59,28 @@ enum Epilogue { kStore = 0, kResidual = 1, kSwiGLU = 2 };
 void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                int M, int N, int K, const int32_t* slot_seg, int capacity, hipStream_t s);
 
+// The QKV projection with RoPE and the cache UNPACK in its epilogue (kQkvRope);
+// N = (H + 2 Hkv) * 128, slot_seg required.
+void qkv_rope_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, int M, int K,
+                   const int32_t* slot_seg, int capacity, const QkvOut& out, hipStream_t s);
+
 // float32 FMA GEMM (kStore / kResidual).  Requires K % 16 == 0.
 void gemm_f32(int epi, const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
               int M, int N, int K, hipStream_t s);
 
 // Attention over segments (independent mask): for every query slot of every work-list
 // tile, softmax(q k^T / sqrt(D)) v over the keys of its own segment at or before it.
-// qkv rows hold [Q (H heads) | K (Hkv heads) | V (Hkv heads)], D = 128.
-void attention_bf16(const void* qkv, int64_t ld, void* out, int64_t ldo, const int32_t* seg_start,
-                    const int32_t* seg_len, const int32_t* qtile_seg, const int32_t* qtile_q0,
-                    int n_qtiles, int H, int Hkv, int D, hipStream_t s);
+// q [slots, ldq] (H heads of D = 128); keys and values of segment s are rows
+// prompt_kv_off[seg_prompt[s]] + j of kc / vc [*, ldkv], zero past the prompt's length.
+void attention_bf16(const void* q, int64_t ldq, const void* kc, const void* vc, int64_t ldkv, void* out,
+                    int64_t ldo, const int32_t* seg_prompt, const int32_t* seg_start, const int32_t* seg_len,
+                    const int32_t* prompt_kv_off, const int32_t* qtile_seg, const int32_t* qtile_q0, int n_qtiles,
+                    int H, int Hkv, hipStream_t s);
 
-// float32 attention, one wavefront per (slot, head); slots outside every span are skipped.
-void attention_f32(const float* qkv, int64_t ld, float* out, int64_t ldo, const int32_t* slot_seg,
-                   const int32_t* seg_start, int T, int H, int Hkv, int D, hipStream_t s);
+// float32 attention, one wavefront per (slot, head), same operands; slots outside every
+// span are skipped.
+void attention_f32(const float* q, int64_t ldq, const float* kc, const float* vc, int64_t ldkv, float* out,
+                   int64_t ldo, const int32_t* slot_seg, const int32_t* seg_prompt, const int32_t* seg_start,
+                   const int32_t* prompt_kv_off, int T, int H, int Hkv, int D, hipStream_t s);
 
 }  // namespace ppk

@@ -4,9 +4,11 @@
 // the kernel sequence on the caller's stream without any host synchronisation:
 //
 //   rope_table; embed (TENSORIZE through the slot map)
-//   per layer: rmsnorm -> QKV GEMM -> RoPE at restart positions -> KV UNPACK scatter ->
-//              attention under the independent mask -> O GEMM (+residual) -> rmsnorm ->
-//              gate/up GEMM with SwiGLU -> down GEMM (+residual)
+//   per layer: rmsnorm -> QKV projection with RoPE at restart positions and the KV UNPACK
+//              fused into its epilogue (bf16; float32 runs GEMM, RoPE and scatter as three
+//              launches) -> attention under the independent mask, keys and values read
+//              from the caches -> O GEMM (+residual) -> rmsnorm -> gate/up GEMM with
+//              SwiGLU -> down GEMM (+residual)
 //   final rmsnorm fused with the hidden-state UNPACK.
 #include <hip/hip_runtime.h>
 
@@ -56,10 +58,10 @@ pp_status validate_config(const pp_config* c) {
     return PP_OK;
 }
 
-// The attention kernel addresses one segment's key rows through a 32-bit buffer range.
+// The attention kernel addresses one prompt's cache rows through a 32-bit buffer range.
 pp_status validate_attention_span(const pp_config* c, const pp_dplan* p) {
-    const int64_t qkv_w = int64_t(c->n_heads + 2 * c->n_kv_heads) * c->head_dim;
-    if (c->dtype == PP_BF16 && (int64_t(p->max_len) + 2 * 64) * qkv_w * 2 > INT32_MAX)
+    const int64_t kvw = int64_t(c->n_kv_heads) * c->head_dim;
+    if (c->dtype == PP_BF16 && (int64_t(p->max_len) + 2 * 64) * kvw * 2 > INT32_MAX)
         return pp::fail(PP_ERR_UNSUPPORTED, "max_len %d too long for the attention kernel at this width",
                         p->max_len);
     return PP_OK;
@@ -75,8 +77,8 @@ pp_status validate_plan(const pp_dplan* p) {
         (p->total_len > 0 && (p->n_qtiles == 0 || p->max_len == 0)))
         return pp::fail(PP_ERR_INVALID_ARG, "inconsistent plan (total_len %d, rows %d x %d, max_len %d)",
                         p->total_len, p->n_rows, p->capacity, p->max_len);
-    if (p->total_len > 0 && (!p->seg_start || !p->seg_len || !p->slot_seg || !p->slot_pos || !p->slot_kv ||
-                             !p->qtile_seg || !p->qtile_q0))
+    if (p->total_len > 0 && (!p->seg_prompt || !p->seg_start || !p->seg_len || !p->prompt_kv_off ||
+                             !p->slot_seg || !p->slot_pos || !p->slot_kv || !p->qtile_seg || !p->qtile_q0))
         return pp::fail(PP_ERR_INVALID_ARG, "a device plan array is NULL");
     return PP_OK;
 }
@@ -96,7 +98,7 @@ Layout layout_of(const pp_config* c, const pp_dplan* p) {
     };
     L.x = take(T * d * 4);
     L.xn = take(T * d * e);
-    L.qkv = take(T * qkv_w * e);
+    L.qkv = take(c->dtype == PP_BF16 ? T * hd * 2 : T * qkv_w * 4);   // bf16: queries only
     L.attn = take(T * hd * e);
     L.act = take(T * F * e);
     L.gu = take(c->dtype == PP_F32 ? T * 2 * F * 4 : 0);
@@ -174,20 +176,21 @@ extern "C" pp_status pp_prefill(const pp_config* cfg, const pp_weights* w, const
         void* kc = static_cast<char*>(k_cache) + l * cache_layer_bytes;
         void* vc = static_cast<char*>(v_cache) + l * cache_layer_bytes;
         ppk::rmsnorm(dt, x, w->attn_norm[l], xn, T, d, eps, s);
-        if (bf)
-            ppk::gemm_bf16(ppk::kStore, xn, d, w->wqkv[l], d, qkv, qkv_w, T, qkv_w, d, plan->slot_seg, C, s);
-        else
-            ppk::gemm_f32(ppk::kStore, static_cast<const float*>(xn), d, static_cast<const float*>(w->wqkv[l]), d,
-                          static_cast<float*>(qkv), qkv_w, T, qkv_w, d, s);
-        ppk::rope_apply(dt, qkv, qkv_w, table, plan->slot_pos, plan->slot_seg, T, H + Hkv, D, s);
-        ppk::kv_scatter(dt, qkv, qkv_w, hd, kvw, kc, vc, plan->slot_kv, T, s);
         if (bf) {
-            ppk::attention_bf16(qkv, qkv_w, attn, hd, plan->seg_start, plan->seg_len, plan->qtile_seg,
-                                plan->qtile_q0, plan->n_qtiles, H, Hkv, D, s);
+            const ppk::QkvOut qo{qkv, hd, kc, vc, kvw, table, plan->slot_pos, plan->slot_kv, H, Hkv};
+            ppk::qkv_rope_bf16(xn, d, w->wqkv[l], d, T, d, plan->slot_seg, C, qo, s);
+            ppk::attention_bf16(qkv, hd, kc, vc, kvw, attn, hd, plan->seg_prompt, plan->seg_start, plan->seg_len,
+                                plan->prompt_kv_off, plan->qtile_seg, plan->qtile_q0, plan->n_qtiles, H, Hkv, s);
             ppk::gemm_bf16(ppk::kResidual, attn, hd, w->wo[l], hd, x, d, T, d, hd, plan->slot_seg, C, s);
         } else {
-            ppk::attention_f32(static_cast<const float*>(qkv), qkv_w, static_cast<float*>(attn), hd, plan->slot_seg,
-                               plan->seg_start, T, H, Hkv, D, s);
+            float* qkv32 = static_cast<float*>(qkv);
+            ppk::gemm_f32(ppk::kStore, static_cast<const float*>(xn), d, static_cast<const float*>(w->wqkv[l]), d,
+                          qkv32, qkv_w, T, qkv_w, d, s);
+            ppk::rope_apply(dt, qkv, qkv_w, table, plan->slot_pos, plan->slot_seg, T, H + Hkv, D, s);
+            ppk::kv_scatter(dt, qkv, qkv_w, hd, kvw, kc, vc, plan->slot_kv, T, s);
+            ppk::attention_f32(qkv32, qkv_w, static_cast<const float*>(kc), static_cast<const float*>(vc), kvw,
+                               static_cast<float*>(attn), hd, plan->slot_seg, plan->seg_prompt, plan->seg_start,
+                               plan->prompt_kv_off, T, H, Hkv, D, s);
             ppk::gemm_f32(ppk::kResidual, static_cast<const float*>(attn), hd, static_cast<const float*>(w->wo[l]),
                           hd, x, d, T, d, hd, s);
         }
@@ -293,6 +296,30 @@ extern "C" pp_status pp_gemm(int32_t dtype, int32_t epilogue, const void* A, int
     return finish("gemm");
 }
 
+extern "C" pp_status pp_qkv_projection(const pp_config* cfg, const pp_dplan* plan, const void* xn,
+                                       const void* wqkv, void* table, void* q_out, void* k_cache, void* v_cache,
+                                       void* stream) {
+    pp::clear_error();
+    if (pp_status st = validate_config(cfg)) return st;
+    if (cfg->dtype != PP_BF16)
+        return pp::fail(PP_ERR_UNSUPPORTED, "the fused QKV projection is bf16 only (float32: pp_gemm, pp_rope, "
+                        "pp_kv_scatter)");
+    if (pp_status st = validate_plan(plan)) return st;
+    const int T = plan->n_rows * plan->capacity;
+    if (T == 0 || plan->total_len == 0) return PP_OK;
+    if (!xn || !wqkv || !table || !q_out || !k_cache || !v_cache)
+        return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
+    (void)hipGetLastError();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int H = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim, d = cfg->d_model;
+    float2* tab = static_cast<float2*>(table);
+    ppk::rope_table(tab, plan->max_len, D, cfg->rope_theta, s);
+    const ppk::QkvOut qo{q_out, int64_t(H) * D, k_cache, v_cache, int64_t(Hkv) * D, tab, plan->slot_pos,
+                         plan->slot_kv, H, Hkv};
+    ppk::qkv_rope_bf16(xn, d, wqkv, d, T, d, plan->slot_seg, plan->capacity, qo, s);
+    return finish("qkv_projection");
+}
+
 extern "C" pp_status pp_rope(const pp_config* cfg, const pp_dplan* plan, void* qkv, void* table, void* stream) {
     pp::clear_error();
     if (pp_status st = validate_config(cfg)) return st;
@@ -325,25 +352,29 @@ extern "C" pp_status pp_kv_scatter(const pp_config* cfg, const pp_dplan* plan, c
     return finish("kv_scatter");
 }
 
-extern "C" pp_status pp_attention(const pp_config* cfg, const pp_dplan* plan, const void* qkv, void* out,
-                                  void* stream) {
+extern "C" pp_status pp_attention(const pp_config* cfg, const pp_dplan* plan, const void* q, int64_t ldq,
+                                  const void* k_cache, const void* v_cache, void* out, void* stream) {
     pp::clear_error();
     if (pp_status st = validate_config(cfg)) return st;
     if (pp_status st = validate_plan(plan)) return st;
     if (pp_status st = validate_attention_span(cfg, plan)) return st;
+    const int H = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim;
+    if (ldq < int64_t(H) * D) return pp::fail(PP_ERR_INVALID_ARG, "ldq %lld < H*D", (long long)ldq);
+    if (cfg->dtype == PP_BF16 && ldq % 8) return pp::fail(PP_ERR_UNSUPPORTED, "bf16 attention needs ldq %% 8 == 0");
     const int T = plan->n_rows * plan->capacity;
     if (T == 0 || plan->total_len == 0) return PP_OK;
-    if (!qkv || !out) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
+    if (!q || !k_cache || !v_cache || !out) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
     (void)hipGetLastError();
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int H = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim;
-    const int qkv_w = (H + 2 * Hkv) * D;
     if (cfg->dtype == PP_BF16)
-        ppk::attention_bf16(qkv, qkv_w, out, H * D, plan->seg_start, plan->seg_len, plan->qtile_seg, plan->qtile_q0,
-                            plan->n_qtiles, H, Hkv, D, s);
+        ppk::attention_bf16(q, ldq, k_cache, v_cache, int64_t(Hkv) * D, out, int64_t(H) * D, plan->seg_prompt,
+                            plan->seg_start, plan->seg_len, plan->prompt_kv_off, plan->qtile_seg, plan->qtile_q0,
+                            plan->n_qtiles, H, Hkv, s);
     else
-        ppk::attention_f32(static_cast<const float*>(qkv), qkv_w, static_cast<float*>(out), H * D, plan->slot_seg,
-                           plan->seg_start, T, H, Hkv, D, s);
+        ppk::attention_f32(static_cast<const float*>(q), ldq, static_cast<const float*>(k_cache),
+                           static_cast<const float*>(v_cache), int64_t(Hkv) * D, static_cast<float*>(out),
+                           int64_t(H) * D, plan->slot_seg, plan->seg_prompt, plan->seg_start, plan->prompt_kv_off,
+                           T, H, Hkv, D, s);
     return finish("attention");
 }
 

@@ -63,9 +63,9 @@ class PPWeights(ctypes.Structure):
 class PPDPlan(ctypes.Structure):
     _fields_ = [("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("n_rows", ctypes.c_int32),
                 ("max_len", ctypes.c_int32), ("total_len", ctypes.c_int32), ("n_qtiles", ctypes.c_int32),
-                ("seg_start", ctypes.c_void_p), ("seg_len", ctypes.c_void_p), ("slot_seg", ctypes.c_void_p),
-                ("slot_pos", ctypes.c_void_p), ("slot_kv", ctypes.c_void_p), ("qtile_seg", ctypes.c_void_p),
-                ("qtile_q0", ctypes.c_void_p)]
+                ("seg_prompt", ctypes.c_void_p), ("seg_start", ctypes.c_void_p), ("seg_len", ctypes.c_void_p),
+                ("prompt_kv_off", ctypes.c_void_p), ("slot_seg", ctypes.c_void_p), ("slot_pos", ctypes.c_void_p),
+                ("slot_kv", ctypes.c_void_p), ("qtile_seg", ctypes.c_void_p), ("qtile_q0", ctypes.c_void_p)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -96,7 +96,8 @@ def lib() -> ctypes.CDLL:
         L.pp_gemm.argtypes = [i32, i32, vp, i64, vp, i64, vp, i64, i32, i32, i32, dpp, vp]
         L.pp_rope.argtypes = [cfgp, dpp, vp, vp, vp]
         L.pp_kv_scatter.argtypes = [cfgp, dpp, vp, vp, vp, vp]
-        L.pp_attention.argtypes = [cfgp, dpp, vp, vp, vp]
+        L.pp_attention.argtypes = [cfgp, dpp, vp, i64, vp, vp, vp, vp]
+        L.pp_qkv_projection.argtypes = [cfgp, dpp, vp, vp, vp, vp, vp, vp, vp]
         L.pp_final_norm_unpack.argtypes = [vp, vp, i32, f32, dpp, vp, vp]
         for name in ("pp_plan_bounds", "pp_pack", "pp_pack_padded", "pp_prefill_workspace_size", "pp_prefill",
                      "pp_embed", "pp_rmsnorm", "pp_gemm", "pp_rope", "pp_kv_scatter", "pp_attention",
@@ -206,7 +207,8 @@ class DevicePlan:
         torch = _torch()
         self.plan = plan
         self.tensors = {n: torch.from_numpy(np.ascontiguousarray(getattr(plan, n))).to(device)
-                        for n in ("seg_start", "seg_len", "slot_seg", "slot_pos", "slot_kv", "qtile_seg", "qtile_q0")}
+                        for n in ("seg_prompt", "seg_start", "seg_len", "prompt_kv_off", "slot_seg", "slot_pos",
+                                  "slot_kv", "qtile_seg", "qtile_q0")}
         self.struct = PPDPlan(k=plan.k, capacity=plan.capacity, n_rows=plan.n_rows, max_len=plan.max_len,
                               total_len=plan.total_len, n_qtiles=plan.n_qtiles,
                               **{n: t.data_ptr() for n, t in self.tensors.items()})
@@ -337,9 +339,15 @@ def pp_kv_scatter(cfg: PPConfig, dplan: DevicePlan, qkv, k_cache, v_cache, strea
                                _stream(stream)), "pp_kv_scatter")
 
 
-def pp_attention(cfg: PPConfig, dplan: DevicePlan, qkv, out, stream=None) -> None:
-    _check(lib().pp_attention(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(qkv), _p(out), _stream(stream)),
-           "pp_attention")
+def pp_qkv_projection(cfg: PPConfig, dplan: DevicePlan, xn, wqkv, table, q_out, k_cache, v_cache,
+                      stream=None) -> None:
+    _check(lib().pp_qkv_projection(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(xn), _p(wqkv), _p(table),
+                                   _p(q_out), _p(k_cache), _p(v_cache), _stream(stream)), "pp_qkv_projection")
+
+
+def pp_attention(cfg: PPConfig, dplan: DevicePlan, q, ldq: int, k_cache, v_cache, out, stream=None) -> None:
+    _check(lib().pp_attention(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(q), ldq, _p(k_cache),
+                              _p(v_cache), _p(out), _stream(stream)), "pp_attention")
 
 
 def pp_final_norm_unpack(x, gain, d: int, eps: float, dplan: DevicePlan, hidden, stream=None) -> None:

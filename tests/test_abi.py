@@ -41,7 +41,7 @@ def test_every_declared_symbol_is_exported(L):
 def test_struct_layouts_match_header():
     assert ctypes.sizeof(pp.PPPlan) == 6 * 4 + 2 * 8 + 10 * 8
     assert ctypes.sizeof(pp.PPConfig) == 10 * 4
-    assert ctypes.sizeof(pp.PPDPlan) == 6 * 4 + 7 * 8
+    assert ctypes.sizeof(pp.PPDPlan) == 6 * 4 + 9 * 8
     assert ctypes.sizeof(pp.PPWeights) == 8 * 8
 
 
@@ -135,8 +135,8 @@ def _cfg(**kw):
 
 def _dplan(**kw):
     base = dict(k=2, capacity=256, n_rows=2, max_len=200, total_len=300, n_qtiles=3,
-                **{n: 0x1000 for n in ("seg_start", "seg_len", "slot_seg", "slot_pos", "slot_kv", "qtile_seg",
-                                       "qtile_q0")})
+                **{n: 0x1000 for n in ("seg_prompt", "seg_start", "seg_len", "prompt_kv_off", "slot_seg",
+                                       "slot_pos", "slot_kv", "qtile_seg", "qtile_q0")})
     base.update(kw)
     return pp.PPDPlan(**base)
 
@@ -151,7 +151,9 @@ def test_workspace_size_and_config_validation(L):
     st_, n = _ws(_cfg(), _dplan())
     assert st_ == pp.PP_OK
     T = 512
-    want = T * 4096 * 4 + T * 4096 * 2 + T * 6144 * 2 + T * 4096 * 2 + T * 14336 * 2 + 200 * 64 * 8
+    # x (f32), xn, q (bf16 keeps only the queries: keys and values go straight to the caches),
+    # attention output, SwiGLU activations, RoPE table
+    want = T * 4096 * 4 + T * 4096 * 2 + T * 4096 * 2 + T * 4096 * 2 + T * 14336 * 2 + 200 * 64 * 8
     assert want <= n <= want + 8 * 256
     assert _ws(_cfg(head_dim=96), _dplan())[0] == pp.PP_ERR_UNSUPPORTED
     assert _ws(_cfg(n_kv_heads=5), _dplan())[0] == pp.PP_ERR_UNSUPPORTED
@@ -165,6 +167,8 @@ def test_workspace_size_and_config_validation(L):
     assert _ws(_cfg(), _dplan(total_len=600))[0] == pp.PP_ERR_INVALID_ARG        # more tokens than slots (512)
     assert _ws(_cfg(), _dplan(max_len=300))[0] == pp.PP_ERR_INVALID_ARG          # longer than a row
     assert _ws(_cfg(), _dplan(slot_kv=0))[0] == pp.PP_ERR_INVALID_ARG            # NULL device array
+    assert _ws(_cfg(), _dplan(prompt_kv_off=0))[0] == pp.PP_ERR_INVALID_ARG
+    assert _ws(_cfg(), _dplan(seg_prompt=0))[0] == pp.PP_ERR_INVALID_ARG
 
 
 def _weights(n_layers):
@@ -199,3 +203,20 @@ def test_prefill_rejects_before_enqueue(L):
     w2, keep2 = _weights(1)
     assert f(ctypes.byref(cfg), ctypes.byref(w2), ctypes.byref(empty), None, None, 0, None, None, None,
              None) == pp.PP_OK
+
+
+def test_step_entry_points_reject_before_enqueue(L):
+    """Host-side argument checks of the fused QKV projection and of attention."""
+    cfg, dp = _cfg(), _dplan()
+    f32 = _cfg(dtype=pp.PP_F32, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=688)
+    q = L.pp_qkv_projection
+    assert q(ctypes.byref(f32), ctypes.byref(dp), 1, 1, 1, 1, 1, 1, None) == pp.PP_ERR_UNSUPPORTED
+    assert q(ctypes.byref(cfg), ctypes.byref(dp), None, 1, 1, 1, 1, 1, None) == pp.PP_ERR_INVALID_ARG
+    assert q(ctypes.byref(cfg), None, 1, 1, 1, 1, 1, 1, None) == pp.PP_ERR_INVALID_ARG
+    a = L.pp_attention
+    assert a(ctypes.byref(cfg), ctypes.byref(dp), 0x1000, 4000, 1, 1, 1, None) == pp.PP_ERR_INVALID_ARG  # ldq < H D
+    assert a(ctypes.byref(cfg), ctypes.byref(dp), 0x1000, 4100, 1, 1, 1, None) == pp.PP_ERR_UNSUPPORTED  # ldq % 8
+    assert a(ctypes.byref(cfg), ctypes.byref(dp), None, 4096, 1, 1, 1, None) == pp.PP_ERR_INVALID_ARG
+    # a prompt too long for the kernel's 32-bit cache addressing is refused up front
+    huge = _dplan(capacity=1100000, n_rows=1, max_len=1100000, total_len=300)   # x 8 KV heads x 256 B > 2 GiB
+    assert a(ctypes.byref(cfg), ctypes.byref(huge), 0x1000, 4096, 1, 1, 1, None) == pp.PP_ERR_UNSUPPORTED

@@ -91,15 +91,24 @@ ATTN_CASES = [
 ]
 
 
-def _attn_ref(plan, qkv, H, Hkv, Dh=128):
+def _attn_inputs(plan, rng, H, Hkv, Dh, scale, dtype):
+    """Queries per slot and per-prompt caches, as the QKV projection leaves them."""
+    mk = (lambda shape: rand_bf16(rng, shape, scale)) if dtype == pp.PP_BF16 else \
+        (lambda shape: (rng.standard_normal(shape) * scale).astype(np.float32))
+    return mk((plan.n_slots, H * Dh)), mk((plan.total_len, Hkv * Dh)), mk((plan.total_len, Hkv * Dh))
+
+
+def _attn_ref(plan, q, kc, vc, H, Hkv, Dh=128):
+    """Per segment: causal attention over its prompt's cache rows, zero keys past the prompt."""
     ref = np.zeros((plan.n_slots, H * Dh))
     for s in range(len(plan.seg_start)):
-        a, n = int(plan.seg_start[s]), int(plan.seg_len[s])
-        rows = qkv[a:a + n].astype(np.float64)
-        q = rows[:, :H * Dh].reshape(n, H, Dh)
-        k = rows[:, H * Dh:(H + Hkv) * Dh].reshape(n, Hkv, Dh)
-        v = rows[:, (H + Hkv) * Dh:].reshape(n, Hkv, Dh)
-        ref[a:a + n] = D.attention(q, k, v, D.causal(n)).reshape(n, H * Dh)
+        a, n, p = int(plan.seg_start[s]), int(plan.seg_len[s]), int(plan.seg_prompt[s])
+        k0, k1 = int(plan.prompt_kv_off[p]), int(plan.prompt_kv_off[p + 1])
+        k = np.zeros((n, Hkv * Dh))
+        v = np.zeros((n, Hkv * Dh))
+        k[:k1 - k0], v[:k1 - k0] = kc[k0:k1], vc[k0:k1]
+        qs = q[a:a + n].astype(np.float64).reshape(n, H, Dh)
+        ref[a:a + n] = D.attention(qs, k.reshape(n, Hkv, Dh), v.reshape(n, Hkv, Dh), D.causal(n)).reshape(n, H * Dh)
     return ref
 
 
@@ -108,12 +117,11 @@ def _attn_ref(plan, qkv, H, Hkv, Dh=128):
 def test_attention_bf16(lengths, cap, H, Hkv, padded):
     plan = pp.pp_pack_padded(lengths) if padded else pp.pp_pack(lengths, cap)
     rng = np.random.default_rng(len(lengths) * 131 + cap)
-    W = (H + 2 * Hkv) * 128
-    qkv = rand_bf16(rng, (plan.n_slots, W), 1.3)
+    q, kc, vc = _attn_inputs(plan, rng, H, Hkv, 128, 1.3, pp.PP_BF16)
     out = torch.full((plan.n_slots, H * 128), float("nan"), dtype=torch.bfloat16, device="cuda")
-    pp.pp_attention(_cfg(H, Hkv), pp.DevicePlan(plan), bf16_dev(qkv), out)
+    pp.pp_attention(_cfg(H, Hkv), pp.DevicePlan(plan), bf16_dev(q), H * 128, bf16_dev(kc), bf16_dev(vc), out)
     got = host64(out)
-    ref = _attn_ref(plan, qkv, H, Hkv)
+    ref = _attn_ref(plan, q, kc, vc, H, Hkv)
     span = plan.slot_seg >= 0
     assert np.all(np.isfinite(got[span]))
     assert np.all(np.isnan(got[~span]))      # rows outside every span are never written
@@ -121,17 +129,82 @@ def test_attention_bf16(lengths, cap, H, Hkv, padded):
     check_bar(f"attention {lengths} H{H}/{Hkv} padded={padded}", got[real], ref[real])
 
 
-def test_attention_f32():
-    lengths, H, Hkv, Dh = [7, 1, 30, 64], 4, 2, 64
-    plan = pp.pp_pack(lengths, 64)
-    rng = np.random.default_rng(11)
-    qkv = rng.standard_normal((plan.n_slots, (H + 2 * Hkv) * Dh)).astype(np.float32)
-    out = torch.zeros((plan.n_slots, H * Dh), dtype=torch.float32, device="cuda")
-    pp.pp_attention(_cfg(H, Hkv, d=256, F=688, dtype=pp.PP_F32, D_=Dh), pp.DevicePlan(plan), f32_dev(qkv), out)
-    ref = _attn_ref(plan, qkv, H, Hkv, Dh)
+def test_attention_bf16_strided_queries():
+    """Queries read from a wider row (ldq > H D), e.g. straight out of a fused QKV buffer."""
+    lengths, H, Hkv = [77, 300, 5], 16, 4
+    plan = pp.pp_pack(lengths, 512)
+    rng = np.random.default_rng(12)
+    q, kc, vc = _attn_inputs(plan, rng, H, Hkv, 128, 1.0, pp.PP_BF16)
+    wide = np.zeros((plan.n_slots, (H + 2 * Hkv) * 128), dtype=np.float32)
+    wide[:, :H * 128] = q
+    out = torch.zeros((plan.n_slots, H * 128), dtype=torch.bfloat16, device="cuda")
+    pp.pp_attention(_cfg(H, Hkv), pp.DevicePlan(plan), bf16_dev(wide), wide.shape[1], bf16_dev(kc), bf16_dev(vc),
+                    out)
     real = plan.slot_kv >= 0
-    mx, _ = report("attention f32", host64(out)[real], ref[real])
+    check_bar("attention strided q", host64(out)[real], _attn_ref(plan, q, kc, vc, H, Hkv)[real])
+
+
+@pytest.mark.parametrize("padded", [False, True])
+def test_attention_f32(padded):
+    lengths, H, Hkv, Dh = [7, 1, 30, 64], 4, 2, 64
+    plan = pp.pp_pack_padded(lengths) if padded else pp.pp_pack(lengths, 64)
+    rng = np.random.default_rng(11)
+    q, kc, vc = _attn_inputs(plan, rng, H, Hkv, Dh, 1.0, pp.PP_F32)
+    out = torch.zeros((plan.n_slots, H * Dh), dtype=torch.float32, device="cuda")
+    pp.pp_attention(_cfg(H, Hkv, d=256, F=688, dtype=pp.PP_F32, D_=Dh), pp.DevicePlan(plan), f32_dev(q), H * Dh,
+                    f32_dev(kc), f32_dev(vc), out)
+    ref = _attn_ref(plan, q, kc, vc, H, Hkv, Dh)
+    real = plan.slot_kv >= 0
+    mx, _ = report(f"attention f32 padded={padded}", host64(out)[real], ref[real])
     assert mx <= 1e-5
+
+
+# ----------------------------------------------------------------------------- fused QKV projection
+QKV_CASES = [
+    # lengths, capacity (None: full batching), H, Hkv, d, theta
+    ([1, 5, 64, 127, 128, 129, 300, 700], 1024, 32, 32, 4096, 10000.0),
+    ([40, 200, 513, 1, 1000], 1024, 32, 8, 4096, 500000.0),
+    ([33, 250, 7], None, 16, 16, 2048, 10000.0),
+]
+
+
+@pytest.mark.parametrize("lengths,cap,H,Hkv,d,theta", QKV_CASES)
+def test_qkv_projection_fused(lengths, cap, H, Hkv, d, theta):
+    """Q, K, V projections, RoPE at restart positions and the cache UNPACK, against the
+    oracle's separate steps in float64."""
+    plan = pp.pp_pack_padded(lengths) if cap is None else pp.pp_pack(lengths, cap)
+    rng = np.random.default_rng([len(lengths), d, H, Hkv])
+    Dh, T = 128, plan.n_slots
+    xn = rand_bf16(rng, (T, d))
+    W = rand_bf16(rng, ((H + 2 * Hkv) * Dh, d), 0.02)
+    q = torch.full((T, H * Dh), float("nan"), dtype=torch.bfloat16, device="cuda")
+    kc = torch.full((plan.total_len, Hkv * Dh), float("nan"), dtype=torch.bfloat16, device="cuda")
+    vc = torch.full_like(kc, float("nan"))
+    table = torch.empty(plan.max_len * 64 * 2, dtype=torch.float32, device="cuda")
+    pp.pp_qkv_projection(_cfg(H, Hkv, d=d, theta=theta), pp.DevicePlan(plan), bf16_dev(xn), bf16_dev(W), table,
+                         q, kc, vc)
+    real = np.nonzero(plan.slot_kv >= 0)[0]
+    proj = xn[real].astype(np.float64) @ W.astype(np.float64).T
+    cos, sin = D.rope_cos_sin(plan.slot_pos[real], Dh, theta)
+    n = len(real)
+    rq = D.rope(proj[:, :H * Dh].reshape(n, H, Dh), cos, sin).reshape(n, H * Dh)
+    rk = D.rope(proj[:, H * Dh:(H + Hkv) * Dh].reshape(n, Hkv, Dh), cos, sin).reshape(n, Hkv * Dh)
+    rv = proj[:, (H + Hkv) * Dh:]
+    got_q = host64(q)[real]
+    kv_rows = plan.slot_kv[real]
+    got_k, got_v = host64(kc), host64(vc)
+    assert np.all(np.isfinite(got_k)) and np.all(np.isfinite(got_v))    # every cache row written
+    for name, got, ref in (("q", got_q, rq), ("k", got_k[kv_rows], rk), ("v", got_v[kv_rows], rv)):
+        assert within_ulps(got, ref, 1.0, 1e-5) <= 1.0, name
+        check_bar(f"qkv projection {name} {lengths} H{H}/{Hkv}", got, ref)
+    # restart: every prompt's first key sits at position 0, where RoPE is the identity
+    slot_of_kv = np.empty(plan.total_len, dtype=np.int64)
+    slot_of_kv[kv_rows] = real
+    first = plan.prompt_kv_off[:-1]
+    s0 = slot_of_kv[first]
+    assert np.all(plan.slot_pos[s0] == 0)
+    k0 = xn[s0].astype(np.float64) @ W[H * Dh:(H + Hkv) * Dh].astype(np.float64).T
+    assert within_ulps(got_k[first], k0, 1.0, 1e-5) <= 1.0
 
 
 # ----------------------------------------------------------------------------- RoPE
