@@ -11,8 +11,13 @@ Prints one JSON line:
   tflops_effective algorithmic FLOP / time (pads and skipped work excluded)
   padded           the same kernels on the full-batching plan (the paper's baseline)
   roofline         the dominant kernel (the gate/up projection GEMM with SwiGLU epilogue),
-                   timed live with HIP events on its stream, against the bf16 MFMA peak
+                   timed live with HIP events on its stream, against the bf16 MFMA peak;
+                   `traffic` is its HBM bytes per launch from the committed counter summary,
+                   reported only while the kernel source still matches the one measured
   cpu_baseline     the CPU oracle timed on a bounded sample of the same workload
+
+--traffic-pass runs only that kernel and a plain copy of known size, for the hardware
+counter passes (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE) that calibrate and measure it.
 """
 import argparse
 import json
@@ -26,6 +31,9 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 METRIC = "effective prefill tokens/s + TFLOP/s (% bf16 MFMA peak) vs padded prefill"
+GEMM_SOURCE = os.path.join(ROOT, "paper_2404_09529_amd", "csrc", "k_gemm_bf16.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_swiglu_llama2-7b-lognormal_traffic.md")
+COPY_BYTES = 1 << 30        # the calibration copy reads and writes 1 GiB
 
 
 def log(msg):
@@ -59,6 +67,60 @@ def time_steps(fn, steps, warmup):
     ms = sorted(a.elapsed_time(b) for a, b in ev)
     return {"ms_mean": sum(ms) / len(ms), "ms_median": ms[len(ms) // 2], "ms_p10": ms[len(ms) // 10],
             "ms_p90": ms[min(len(ms) - 1, (9 * len(ms)) // 10)], "wall_s": wall}
+
+
+def source_sha256(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per launch of the gate/up GEMM from the committed counter summary (a line
+    `record: {json}`), or None when there is none or the kernel source has changed since."""
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            line = next(l for l in f if l.startswith("record: "))
+        rec = json.loads(line[len("record: "):])
+    except (OSError, StopIteration, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != source_sha256(GEMM_SOURCE):
+        return None
+    return rec
+
+
+def traffic_pass(args):
+    """The gate/up GEMM alone on the workload's packed plan (random bf16 operands: traffic does
+    not depend on the values), then a float32 copy of COPY_BYTES through a plain elementwise
+    kernel, whose counter readings calibrate the GEMM's."""
+    import torch
+
+    from paper_2404_09529_amd import prepack as pp
+    from paper_2404_09529_amd import workloads as W
+
+    wl = W.workload(args.workload)
+    lengths = W.draw_lengths(wl, args.seed)
+    plan = pp.pp_pack(lengths, wl.capacity)
+    dplan = pp.DevicePlan(plan)
+    shape = wl.shape
+    T, d, F = plan.n_slots, shape.d_model, shape.ffn_dim
+    gen = torch.Generator(device="cuda").manual_seed(1)
+    A = torch.randn((T, d), generator=gen, device="cuda").to(torch.bfloat16)
+    Wgu = (torch.randn((2 * F, d), generator=gen, device="cuda") * 0.02).to(torch.bfloat16)
+    C = torch.empty((T, F), dtype=torch.bfloat16, device="cuda")
+    for _ in range(args.kernel_launches):
+        pp.pp_gemm(pp.PP_BF16, pp.PP_EPI_SWIGLU, A, d, Wgu, d, C, F, T, 2 * F, d, dplan)
+    torch.cuda.synchronize()
+    del A, Wgu, C
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"traffic_pass": wl.name, "gemm_launches": args.kernel_launches, "T": T, "d": d, "F": F,
+                      "total_len": int(lengths.sum()), "copy_read_bytes": COPY_BYTES,
+                      "copy_write_bytes": COPY_BYTES, "kernel_source_sha256": source_sha256(GEMM_SOURCE)}),
+          flush=True)
 
 
 def cpu_baseline(case, budget_s):
@@ -100,6 +162,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--kernel-launches", type=int, default=20)
+    ap.add_argument("--traffic-pass", action="store_true",
+                    help="run only the dominant kernel and the calibration copy (for counter passes)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -116,6 +180,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     pp.lib()
     torch.cuda.set_device(0)
+    if args.traffic_pass:
+        traffic_pass(args)
+        return
 
     t = time.perf_counter()
     case = W.make_case(args.workload, args.seed)
@@ -159,6 +226,8 @@ def main():
     achieved = k_flops / (kt["ms_mean"] / 1e3) / 1e12
     del A, Cb
     log(f"gate/up GEMM: {kt['ms_mean']:.3f} ms/launch, {achieved:.1f} TFLOP/s algorithmic")
+    traffic = recorded_traffic()
+    k_bytes = 2 * (case.total_len * d + 2 * F * d + case.total_len * F)   # A, W once; C written once
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -174,9 +243,11 @@ def main():
         "pack_ms": round(pack_ms, 4), "plan_upload_ms": round(upload_ms, 3),
         "roofline": {"kernel": "gemm_bf16_kernel<kSwiGLU> (gate/up projection)", "bound": "mfma",
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
                      "ms_per_launch": round(kt["ms_mean"], 4),
-                     "algorithmic_flop_per_launch": k_flops},
+                     "algorithmic_flop_per_launch": k_flops, "algorithmic_bytes_per_launch": k_bytes,
+                     "traffic_source": None if traffic is None else os.path.relpath(TRAFFIC_SUMMARY, ROOT)},
     }
     del step
     torch.cuda.empty_cache()
