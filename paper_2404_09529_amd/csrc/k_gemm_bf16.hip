@@ -21,12 +21,14 @@
 // accumulators, with queries stored to the packed batch and keys and values stored straight
 // into the per-prompt caches (the UNPACK of Algorithm 1).
 //
-// Scheduling: a launch has far more tiles than the 256 CUs.  Workgroups are dealt to the
-// 8 XCDs round-robin, so the linear workgroup id is remapped to make each XCD's
-// workgroups a contiguous range of tiles, and tiles are ordered in groups of 4 M-tiles
-// sweeping N, so the tiles resident on one XCD share activation and weight panels in its
-// L2 (measured ~80% L2 hits on the 7B shapes).  M-tiles made only of row-tail padding are skipped (packed batches only carry pads
-// at row tails, section 3.1).
+// Scheduling: persistent, one workgroup per CU.  Workgroups are dealt to the 8 XCDs
+// round-robin, so XCD x runs workgroups x, x + 8, ...; each XCD owns a contiguous block of
+// M-tiles ordered in groups of up to 8 M-tiles sweeping N, and its workgroups take that list
+// in strides of their count, so the 32 tiles resident on an XCD always form one compact
+// block started together.  Each tile also prefetches a quarter of its next K slices into L2
+// (the sharers of a panel pick different quarters), so most LDS fills hit L2.  M-tiles made
+// only of row-tail padding are skipped (packed batches only carry pads at row tails,
+// section 3.1).
 #include "device.h"
 #include "kernels.h"
 
@@ -38,6 +40,9 @@ constexpr int ROW_B = BK * 2;           // LDS row: 128 bytes = 8 chunks of 16 b
 constexpr int OP_B = BM * ROW_B;        // one operand tile in LDS (32 KB)
 constexpr int STAGE_B = 2 * OP_B;       // A tile then B tile (64 KB); two stages = 128 KB
 constexpr int LOADS = BM * ROW_B / 1024 / 4;  // 1 KB direct-to-LDS loads per wavefront per stage (8)
+constexpr int PF_DIST = 2;              // K steps between an L2 prefetch and the load it serves
+constexpr int PF_LDS = 2 * STAGE_B;     // 2 x 256 B of LDS that prefetches land in (never read)
+constexpr int LDS_BYTES = PF_LDS + 512;
 // Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
 constexpr int kRsrcWord3 = 0x00020000;
 
@@ -61,150 +66,12 @@ __device__ __forceinline__ void barrier() {
     __builtin_amdgcn_sched_barrier(0);
 }
 
+// Epilogue of one tile: the lane holds, for activation rows m (two, one per j), runs of 4
+// consecutive n of four 32-column blocks.
 template <int EPI>
-__global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ A, int64_t lda,
-                                                       const bf16* __restrict__ B, int64_t ldb,
-                                                       void* __restrict__ Cv, int64_t ldc, int M, int K,
-                                                       const int32_t* __restrict__ slot_seg, int capacity,
-                                                       int tiles_m, int tiles_n, ppk::QkvOut qo) {
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
-
-    // ---- which tile.  Workgroups are dealt to the 8 XCDs round-robin (XCD = id % 8).  XCD x
-    // owns the contiguous block of M-tiles [x pm, x pm + pm) and walks it in groups of at
-    // most 8 M-tiles, each group sweeping all N-tiles.  Every XCD starts at N-tile 0 at the
-    // same time and advances at the same rate, so the weight panels are fetched from HBM
-    // once into the last-level cache and shared by all XCDs, while each XCD's activation
-    // panels stay resident; the ~32 tiles an XCD runs at once (about 8 M x 4 N) share
-    // panels in its L2.  Workgroups past an XCD's block exit at once.
-    const int g = blockIdx.x;
-    const int xcd = g & 7, local = g >> 3;
-    const int pm = (tiles_m + 7) / 8;
-    const int m_begin = xcd * pm, m_cnt = min(pm, tiles_m - m_begin);
-    if (m_cnt <= 0 || local >= m_cnt * tiles_n) return;
-    const int n_groups = (m_cnt + 7) / 8, gm = (m_cnt + n_groups - 1) / n_groups;
-    const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
-    const int first = group * gm, gsz = min(m_cnt - first, gm);
-    const int mt = m_begin + first + within % gsz;
-    const int nt = within / gsz;
-    const int m0 = mt * BM, n0 = nt * BN;
-    if (!tile_active(slot_seg, capacity, m0, M)) return;
-
-    // ---- direct global -> LDS loads.  A stage holds the A tile then the B tile, 8 chunks of
-    // 16 bytes per row.  Load t of wavefront w fills 1 KB = rows 8 j .. 8 j + 7 of its operand
-    // (j = (w % 4) * 8 + t; wavefronts 0-3 load A, 4-7 load B); lane l lands at physical chunk
-    // l % 8 of row 8 j + l / 8, so it fetches the logical chunk that the swizzle puts there.
-    // Every quad of lanes reads one aligned 64-byte half of a row.  Rows of A past M read as
-    // zero (the descriptor ends at row min(M, m0 + 256)); every access is inside its buffer.
-    const int a_rows = min(M - m0, BM);
-    const bool load_b = wave >= 4;
-    const __amdgpu_buffer_rsrc_t rsrc = load_b
-        ? __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(B + int64_t(n0) * ldb), 0,
-                                            static_cast<int>(BN * ldb * 2), kRsrcWord3)
-        : __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A + int64_t(m0) * lda), 0,
-                                            static_cast<int>(a_rows * lda * 2), kRsrcWord3);
-    const int64_t ld = load_b ? ldb : lda;
-    int voff[LOADS];
-#pragma unroll
-    for (int t = 0; t < LOADS; ++t) {
-        const int row = 8 * ((wave & 3) * LOADS + t) + lane / 8;
-        voff[t] = static_cast<int>(row * ld * 2) + 16 * ((lane & 7) ^ swz(row));
-    }
-    const int lds_op = load_b ? OP_B : 0;
-    auto issue_loads = [&](int kt) {
-        char* stage = smem + (kt & 1) * STAGE_B + lds_op;
-#pragma unroll
-        for (int t = 0; t < LOADS; ++t) {
-            lds_void* dst = (lds_void*)(stage + ((wave & 3) * LOADS + t) * 1024);   // generic -> LDS
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[t], kt * BK * 2, 0, 0);
-        }
-    };
-
-    // ---- wavefront sub-tile: 128 (N) x 64 (M) = 4 x 2 MFMA blocks of 32 x 32
-    const int wn = wave & 1, wm = wave >> 1;
-    const int grp = wave >> 2;               // waves w and w + 4 share a SIMD
-    const int fr = lane & 31, fh = lane >> 5;
-    f32x16 acc[4][2];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-
-    // fragment addresses.  Row r = base + 32 i + fr of either operand has swizzle
-    // f(r) = g ^ 4 (i & 1) with g = ((fr & 7) ^ (fr >> 3)) & 7 (base is a multiple of 64), so
-    // the physical chunk of logical chunk 2 ks + fh is (2 (ks ^ 2 (i & 1))) ^ (fh ^ g): four
-    // per-lane offsets cover every (ks, i); the block stride (32 rows = 4 KB) is immediate.
-    const int gsw = ((fr & 7) ^ (fr >> 3)) & 7;
-    const int x = fh ^ gsw;
-    int a_lds[4], b_lds[4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        a_lds[m] = (wm * 64 + fr) * ROW_B + 16 * ((2 * m) ^ x);
-        b_lds[m] = OP_B + (wn * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
-    }
-    bf16x8 fw[BK / 16][4], fa[BK / 16][2];
-    auto read_frags = [&](int kt) {
-        const char* stage = smem + (kt & 1) * STAGE_B;
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                fw[ks][i] = *reinterpret_cast<const bf16x8*>(stage + b_lds[ks ^ (2 * (i & 1))] + i * 32 * ROW_B);
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                fa[ks][j] = *reinterpret_cast<const bf16x8*>(stage + a_lds[ks ^ (2 * (j & 1))] + j * 32 * ROW_B);
-        }
-    };
-    auto mfmas = [&]() {
-        __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[ks][i], fa[ks][j], acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_s_setprio(0);
-    };
-
-    // ---- ping-pong over K.  Group 0 runs [memory, MFMA] phases; group 1 runs the same one
-    // phase later, so on every SIMD one wavefront issues MFMAs while the other reads LDS.
-    // Tile kt+1 is requested in phase 2kt (group 0 in its memory phase, group 1 at the end
-    // of its MFMA phase) and waited for at the end of phase 2kt+1; a stage is refilled only
-    // after both groups have read it.  Both groups execute 2 nk + 2 barriers.
-    const int nk = K / BK;
-    issue_loads(0);
-    __builtin_amdgcn_s_waitcnt(0);
-    barrier();
-    if (grp == 0) {
-        for (int kt = 0; kt < nk; ++kt) {
-            read_frags(kt);
-            if (kt + 1 < nk) issue_loads(kt + 1);        // after the LDS reads: they start first
-            __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
-            barrier();
-            mfmas();
-            __builtin_amdgcn_s_waitcnt(0x0f70);          // vmcnt(0): this group's part of tile kt+1
-            barrier();
-        }
-        barrier();
-    } else {
-        if (nk > 1) issue_loads(1);
-        barrier();
-        for (int kt = 0; kt < nk; ++kt) {
-            read_frags(kt);
-            __builtin_amdgcn_s_waitcnt(0);               // fragments, and this group's part of tile kt+1
-            barrier();
-            mfmas();
-            // issued after the MFMA burst so the load issue does not delay it; tile kt+2 goes
-            // to the stage both groups finished reading in phases 2kt and 2kt+1, and is
-            // waited for at the end of this group's next memory phase (phase 2kt+3)
-            if (kt + 2 < nk) issue_loads(kt + 2);
-            barrier();
-        }
-    }
-
-    // ---- epilogue: lane holds, for activation row m, runs of 4 consecutive n
+__device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], void* __restrict__ Cv, int64_t ldc, int M,
+                                         int m0, int n0, int wm, int wn, int fr, int fh,
+                                         const int32_t* __restrict__ slot_seg, const ppk::QkvOut& qo) {
     if constexpr (EPI == ppk::kQkvRope) {
         // The wavefront's 128 columns are exactly one head (tiles start at multiples of 256),
         // and the rotate-half partners c and c + 64 are accumulator blocks i and i + 2 of the
@@ -301,13 +168,185 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
     }
 }
 
+template <int EPI>
+__global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ A, int64_t lda,
+                                                       const bf16* __restrict__ B, int64_t ldb,
+                                                       void* __restrict__ Cv, int64_t ldc, int M, int K,
+                                                       const int32_t* __restrict__ slot_seg, int capacity,
+                                                       int tiles_m, int tiles_n, ppk::QkvOut qo) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
+
+    // ---- persistent schedule.  Workgroups are dealt to the 8 XCDs round-robin (XCD = id % 8)
+    // and the grid holds one workgroup per CU, so XCD x runs workgroups x, x + 8, ... one per
+    // CU.  XCD x owns the contiguous block of M-tiles [x pm, x pm + pm), ordered in groups of
+    // at most 8 M-tiles, each group sweeping all N-tiles; its workgroups take that list in
+    // strides of their count.  The tiles resident on an XCD at any time are therefore one
+    // compact block of the list (about 8 M x 4 N tiles) started together, at the same K step:
+    // each 64-wide K slice of an activation or weight panel is fetched into the XCD's L2 once
+    // and read there by every tile of the block.  Every XCD sweeps N at the same rate, so the
+    // weight panels are also shared through the last-level cache.
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, n_slots = gridDim.x >> 3;
+    const int pm = (tiles_m + 7) / 8;
+    const int m_begin = xcd * pm, m_cnt = min(pm, tiles_m - m_begin);
+    if (m_cnt <= 0) return;
+    const int n_groups = (m_cnt + 7) / 8, gm = (m_cnt + n_groups - 1) / n_groups;
+    const int n_local = m_cnt * tiles_n;
+
+    // ---- direct global -> LDS loads.  A stage holds the A tile then the B tile, 8 chunks of
+    // 16 bytes per row.  Load t of wavefront w fills 1 KB = rows 8 j .. 8 j + 7 of its operand
+    // (j = (w % 4) * 8 + t; wavefronts 0-3 load A, 4-7 load B); lane l lands at physical chunk
+    // l % 8 of row 8 j + l / 8, so it fetches the logical chunk that the swizzle puts there.
+    // Every quad of lanes reads one aligned 64-byte half of a row.  Rows of A past M read as
+    // zero (the descriptor ends at row min(M, m0 + 256)); every access is inside its buffer.
+    const bool load_b = wave >= 4;
+    const int64_t ld = load_b ? ldb : lda;
+    int voff[LOADS];
+#pragma unroll
+    for (int t = 0; t < LOADS; ++t) {
+        const int row = 8 * ((wave & 3) * LOADS + t) + lane / 8;
+        voff[t] = static_cast<int>(row * ld * 2) + 16 * ((lane & 7) ^ swz(row));
+    }
+    const int lds_op = load_b ? OP_B : 0;
+    // L2 prefetch: wavefronts 0 and 4 each touch one 64-row quarter of their operand's K
+    // slice PF_DIST steps ahead, one 128-byte line (a row's 64 K values) per lane.
+    const bool pf_wave = (wave & 3) == 0;
+
+    // ---- wavefront sub-tile: 128 (N) x 64 (M) = 4 x 2 MFMA blocks of 32 x 32
+    const int wn = wave & 1, wm = wave >> 1;
+    const int grp = wave >> 2;               // waves w and w + 4 share a SIMD
+    const int fr = lane & 31, fh = lane >> 5;
+
+    // fragment addresses.  Row r = base + 32 i + fr of either operand has swizzle
+    // f(r) = g ^ 4 (i & 1) with g = ((fr & 7) ^ (fr >> 3)) & 7 (base is a multiple of 64), so
+    // the physical chunk of logical chunk 2 ks + fh is (2 (ks ^ 2 (i & 1))) ^ (fh ^ g): four
+    // per-lane offsets cover every (ks, i); the block stride (32 rows = 4 KB) is immediate.
+    const int gsw = ((fr & 7) ^ (fr >> 3)) & 7;
+    const int x = fh ^ gsw;
+    int a_lds[4], b_lds[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        a_lds[m] = (wm * 64 + fr) * ROW_B + 16 * ((2 * m) ^ x);
+        b_lds[m] = OP_B + (wn * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
+    }
+    const int nk = K / BK;
+
+    for (int local = slot; local < n_local; local += n_slots) {
+        const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
+        const int first = group * gm, gsz = min(m_cnt - first, gm);
+        const int mt = m_begin + first + within % gsz;
+        const int nt = within / gsz;
+        const int m0 = mt * BM, n0 = nt * BN;
+        if (!tile_active(slot_seg, capacity, m0, M)) continue;
+
+        const int a_rows = min(M - m0, BM);
+        const __amdgpu_buffer_rsrc_t rsrc = load_b
+            ? __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(B + int64_t(n0) * ldb), 0,
+                                                static_cast<int>(BN * ldb * 2), kRsrcWord3)
+            : __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A + int64_t(m0) * lda), 0,
+                                                static_cast<int>(a_rows * lda * 2), kRsrcWord3);
+        // The tiles of a block that share an A panel have consecutive nt, those sharing a B
+        // panel consecutive mt, so between them they prefetch every quarter once.
+        const int pf_off = static_cast<int>(((load_b ? (mt & 3) : (nt & 3)) * 64 + lane) * ld * 2);
+        auto issue_loads = [&](int kt) {
+            char* stage = smem + (kt & 1) * STAGE_B + lds_op;
+#pragma unroll
+            for (int t = 0; t < LOADS; ++t) {
+                lds_void* dst = (lds_void*)(stage + ((wave & 3) * LOADS + t) * 1024);   // generic -> LDS
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[t], kt * BK * 2, 0, 0);
+            }
+            if (pf_wave) {
+                // always issued (the slice index is clamped), so these wavefronts always have
+                // exactly one younger load outstanding behind a stage's loads
+                const int kp = min(kt + PF_DIST, nk - 1);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(smem + PF_LDS + (wave >> 2) * 256), 4,
+                                                         pf_off, kp * BK * 2, 0, 0);
+            }
+        };
+
+        f32x16 acc[4][2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+        bf16x8 fw[BK / 16][4], fa[BK / 16][2];
+        auto read_frags = [&](int kt) {
+            const char* stage = smem + (kt & 1) * STAGE_B;
+#pragma unroll
+            for (int ks = 0; ks < BK / 16; ++ks) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    fw[ks][i] = *reinterpret_cast<const bf16x8*>(stage + b_lds[ks ^ (2 * (i & 1))] + i * 32 * ROW_B);
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    fa[ks][j] = *reinterpret_cast<const bf16x8*>(stage + a_lds[ks ^ (2 * (j & 1))] + j * 32 * ROW_B);
+            }
+        };
+        auto mfmas = [&]() {
+            __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+            for (int ks = 0; ks < BK / 16; ++ks)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[ks][i], fa[ks][j], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_s_setprio(0);
+        };
+
+        // ---- ping-pong over K.  Group 0 runs [memory, MFMA] phases; group 1 runs the same
+        // one phase later, so on every SIMD one wavefront issues MFMAs while the other reads
+        // LDS.  Tile kt+1 is requested in phase 2kt (group 0 in its memory phase, group 1 at
+        // the end of its MFMA phase) and waited for at the end of phase 2kt+1; a stage is
+        // refilled only after both groups have read it.  Both groups execute 2 nk + 2
+        // barriers, and every LDS read of the tile has completed before the last one, so the
+        // next tile may refill either stage right after it.
+        issue_loads(0);
+        __builtin_amdgcn_s_waitcnt(0);
+        barrier();
+        if (grp == 0) {
+            for (int kt = 0; kt < nk; ++kt) {
+                read_frags(kt);
+                if (kt + 1 < nk) issue_loads(kt + 1);        // after the LDS reads: they start first
+                __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
+                barrier();
+                mfmas();
+                // this group's part of tile kt+1: vmcnt(0), or vmcnt(1) behind the prefetch
+                if (pf_wave) __builtin_amdgcn_s_waitcnt(0x0f71);
+                else __builtin_amdgcn_s_waitcnt(0x0f70);
+                barrier();
+            }
+            barrier();
+        } else {
+            if (nk > 1) issue_loads(1);
+            barrier();
+            for (int kt = 0; kt < nk; ++kt) {
+                read_frags(kt);
+                // fragments, and this group's part of tile kt+1 (vmcnt(1) behind the prefetch)
+                if (pf_wave) __builtin_amdgcn_s_waitcnt(0x0071);
+                else __builtin_amdgcn_s_waitcnt(0x0070);
+                barrier();
+                mfmas();
+                // issued after the MFMA burst so the load issue does not delay it; tile kt+2
+                // goes to the stage both groups finished reading in phases 2kt and 2kt+1, and
+                // is waited for at the end of this group's next memory phase (phase 2kt+3)
+                if (kt + 2 < nk) issue_loads(kt + 2);
+                barrier();
+            }
+        }
+        epilogue<EPI>(acc, Cv, ldc, M, m0, n0, wm, wn, fr, fh, slot_seg, qo);
+    }
+    __builtin_amdgcn_s_waitcnt(0);   // no prefetch may still be writing LDS when the workgroup ends
+}
+
 }  // namespace
 
 namespace ppk {
 
 namespace {
 
-constexpr size_t kLds = 2 * STAGE_B;
+constexpr size_t kLds = LDS_BYTES;
 
 template <int EPI>
 void launch(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc, int M, int N, int K,
@@ -319,7 +358,16 @@ void launch(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int
     }();
     (void)attr;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
-    const dim3 grid(8 * ((tiles_m + 7) / 8) * tiles_n);   // XCD-blocked order; extras exit
+    // one workgroup per CU (each needs 128 KB of LDS, so a CU holds one), a multiple of 8 so
+    // that every XCD runs the same number; never more workgroups than tiles
+    static const int n_cu = [] {
+        int dev = 0, n = 0;
+        (void)hipGetDevice(&dev);
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8) n = 8;
+        return n / 8 * 8;
+    }();
+    const int per_xcd = ((tiles_m + 7) / 8) * tiles_n;
+    const dim3 grid(8 * min(n_cu / 8, per_xcd));
     gemm_bf16_kernel<EPI><<<grid, NT, kLds, s>>>(static_cast<const bf16*>(A), lda, static_cast<const bf16*>(B),
                                                 ldb, C, ldc, M, K, slot_seg, capacity, tiles_m, tiles_n, qo);
 }
