@@ -141,6 +141,51 @@ def test_empty_batch_is_a_noop():
 
 
 # ----------------------------------------------------------------------------- full size, sampled
+def _full_size_sampled(wid, picks_of, name):
+    """The workload at full size (every prompt, every layer, its row length) through
+    pp_prefill; the oracle recomputes a few prompts from scratch and the GPU's cache rows and
+    hidden states for them are gated against the ideal-bf16 floor."""
+    print(f"[parity] {name}: drawing the workload", flush=True)
+    case = W.make_case(wid, 0)
+    plan = pp.pp_pack(case.lengths, case.capacity)
+    print(f"[parity] {name}: L={case.total_len} k={len(case.lengths)} rows={plan.n_rows} x {plan.capacity}, "
+          f"layers={case.shape.n_layers}; running pp_prefill", flush=True)
+    gpu = gpu_prefill(case, plan)
+    picks = picks_of(case.lengths)
+    print(f"[parity] {name}: sampled prompts {picks} lengths {case.lengths[picks].tolist()}; oracle", flush=True)
+    rows = _rows(case, picks)
+    ref = _oracle(case, prompts=picks)
+    floor = _floor(case, prompts=picks)
+    n = case.shape.n_layers
+    _gate(name, _check_bar(name, gpu, ref, n, rows), _check_bar(name + " floor", floor, ref, n, rows))
+    assert np.all(np.isfinite(gpu[0]))
+    for l in range(n):
+        assert np.all(np.isfinite(gpu[1][l])) and np.all(np.isfinite(gpu[2][l]))
+
+
+def _short_median_mid(lengths, cap_tokens=512):
+    """The shortest prompt, the median one, and the longest one of at most cap_tokens."""
+    order = np.argsort(lengths, kind="stable")
+    mid = [int(i) for i in order if lengths[i] <= cap_tokens][-1]
+    return sorted({int(order[0]), int(order[len(order) // 2]), mid})
+
+
+@pytest.mark.timeout(600)
+def test_full_size_7b_bimodal_sampled_prompts():
+    _full_size_sampled(3, _short_median_mid, "7B bimodal full size")
+
+
+@pytest.mark.timeout(600)
+def test_full_size_8b_gqa_sampled_prompts():
+    _full_size_sampled(4, _short_median_mid, "8B GQA full size")
+
+
+@pytest.mark.timeout(600)
+def test_full_size_1b3_long_sampled_prompts():
+    """24 layers, two rows of 32,768 slots, one prompt filling a row on its own."""
+    _full_size_sampled(5, lambda l: _short_median_mid(l, 640), "1.3B long full size")
+
+
 def test_full_size_7b_lognormal_sampled_prompts():
     """The benchmark's own workload and launch configuration (64 prompts, 4 layers, rows of
     4096); the oracle recomputes three prompts from scratch (the shortest, a median one and

@@ -129,6 +129,32 @@ def test_attention_bf16(lengths, cap, H, Hkv, padded):
     check_bar(f"attention {lengths} H{H}/{Hkv} padded={padded}", got[real], ref[real])
 
 
+@pytest.mark.parametrize("n,H,Hkv", [(32768, 16, 16), (8192, 32, 8)])
+def test_attention_bf16_maximum_length(n, H, Hkv):
+    """One segment of the longest prompt a workload holds (a row of 32,768 slots for the 1.3B
+    shape; 8,192 with GQA 32/8): sampled query rows, each against the oracle's attention over
+    all of its keys, first and last rows and every tile boundary around them included."""
+    lengths = [n]
+    plan = pp.pp_pack(lengths, n)
+    rng = np.random.default_rng([n, H, Hkv])
+    q, kc, vc = _attn_inputs(plan, rng, H, Hkv, 128, 1.3, pp.PP_BF16)
+    out = torch.empty((plan.n_slots, H * 128), dtype=torch.bfloat16, device="cuda")
+    pp.pp_attention(_cfg(H, Hkv, d=H * 128), pp.DevicePlan(plan), bf16_dev(q), H * 128, bf16_dev(kc), bf16_dev(vc),
+                    out)
+    got = host64(out)
+    rows = set(rng.choice(n, size=40, replace=False).tolist()) | {0, 1, 63, 64, 127, 128, n - 129, n - 128, n - 1}
+    rows = np.array(sorted(rows))
+    ref = np.zeros((len(rows), H * 128))
+    for r_i, t in enumerate(rows):
+        # query t against its keys 0..t (the causal row of the segment), one query at a time
+        qs = q[t].astype(np.float64).reshape(1, H, 128)
+        ks = kc[:t + 1].astype(np.float64).reshape(t + 1, Hkv, 128)
+        vs = vc[:t + 1].astype(np.float64).reshape(t + 1, Hkv, 128)
+        ref[r_i] = D.attention(qs, ks, vs, np.ones((1, t + 1), dtype=bool)).reshape(H * 128)
+    assert np.all(np.isfinite(got))
+    check_bar(f"attention one segment of {n} H{H}/{Hkv}", got[rows], ref)
+
+
 def test_attention_bf16_strided_queries():
     """Queries read from a wider row (ldq > H D), e.g. straight out of a fused QKV buffer."""
     lengths, H, Hkv = [77, 300, 5], 16, 4
