@@ -89,6 +89,18 @@ def recorded_traffic():
     return rec
 
 
+def calibration_copy():
+    """A float32 copy of COPY_BYTES through a plain elementwise kernel (dst = src * 1.0), run
+    three times: hardware byte counters read on it calibrate the same counters elsewhere."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def traffic_pass(args):
     """The gate/up GEMM alone on the workload's packed plan (random bf16 operands: traffic does
     not depend on the values), then a float32 copy of COPY_BYTES through a plain elementwise
@@ -112,11 +124,7 @@ def traffic_pass(args):
         pp.pp_gemm(pp.PP_BF16, pp.PP_EPI_SWIGLU, A, d, Wgu, d, C, F, T, 2 * F, d, dplan)
     torch.cuda.synchronize()
     del A, Wgu, C
-    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
-    dst = torch.empty_like(src)
-    for _ in range(3):
-        torch.mul(src, 1.0, out=dst)
-    torch.cuda.synchronize()
+    calibration_copy()
     print(json.dumps({"traffic_pass": wl.name, "gemm_launches": args.kernel_launches, "T": T, "d": d, "F": F,
                       "total_len": int(lengths.sum()), "copy_read_bytes": COPY_BYTES,
                       "copy_write_bytes": COPY_BYTES, "kernel_source_sha256": source_sha256(GEMM_SOURCE)}),
@@ -164,6 +172,8 @@ def main():
     ap.add_argument("--kernel-launches", type=int, default=20)
     ap.add_argument("--traffic-pass", action="store_true",
                     help="run only the dominant kernel and the calibration copy (for counter passes)")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="end with the calibration copy (for byte-counter passes over the whole step)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -273,6 +283,8 @@ def main():
         out["cpu_baseline"] = cpu_baseline(case, args.cpu_budget_s)
         log(f"cpu oracle: {out['cpu_baseline']['value']:.1f} tokens/s on {out['cpu_baseline']['cores']} threads")
 
+    if args.calibration_copy:
+        calibration_copy()
     print(json.dumps(out), flush=True)
 
 
