@@ -144,6 +144,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db) o[db] = f32x16{};
     float m_i = -1e30f, l_i = 0.f;
+    const float lazy = 8.0f / scale_log2;             // 8 in log2 units, as a raw-score margin
 
     issue(0);
     for (int kt = 0; kt < nkt; ++kt) {
@@ -153,67 +154,94 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
         if (kt + 1 < nkt) issue(kt + 1);
         const char* stage = smem + (kt & 1) * STAGE_B;
         const int kb = kt * BKV;                       // first key of the tile
-        if (kb <= wq_hi) {
-            f32x16 s[2] = {f32x16{}, f32x16{}};
+        // every wavefront takes part in every key tile: one whose queries all precede the tile
+        // sees only masked scores (p = 0, corr = 1) and leaves o and l unchanged
+        // all K fragments of the tile first, then the 16 score MFMAs
+        bf16x8 kf[HD / 16][2];
 #pragma unroll
-            for (int ks = 0; ks < HD / 16; ++ks) {
+        for (int ks = 0; ks < HD / 16; ++ks)
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(stage + k_lds + b * 32 * ROW +
-                                                                       16 * ((2 * ks) ^ kx));
-                    s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[b], 0, 0, 0);
+            for (int b = 0; b < 2; ++b)
+                kf[ks][b] = *reinterpret_cast<const bf16x8*>(stage + k_lds + b * 32 * ROW + 16 * ((2 * ks) ^ kx));
+        __builtin_amdgcn_sched_barrier(0);
+        f32x16 s[2];
+#pragma unroll
+        for (int ks = 0; ks < HD / 16; ++ks)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][b], qf[ks], ks == 0 ? f32x16{} : s[b], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        // the V operands of the whole tile are requested now, so their LDS latency hides behind
+        // the softmax.  Transposing read r of sub-step sub, d block db: this lane supplies the
+        // address of key row sub*16 + 8 r + vrow and d columns db*32 + vd .. +3 and receives
+        // 4 consecutive keys of one d.
+        bf16x8 vf[BKV / 16][HD / 32];
+#pragma unroll
+        for (int sub = 0; sub < BKV / 16; ++sub)
+#pragma unroll
+            for (int db = 0; db < HD / 32; ++db) {
+                s16x4 v2[2];
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int row = sub * 16 + 8 * r + vrow;
+                    const int d = db * 32 + vd;
+                    const char* p = stage + TILE_B + row * ROW + 16 * ((d >> 3) ^ vs) + (d & 7) * 2;
+                    v2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));   // generic -> LDS
                 }
+                vf[sub][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
             }
-            const bool need_mask = kb + BKV - 1 > wq_lo || kb + BKV > n_kv;
-            float mx = -INFINITY;
+        __builtin_amdgcn_sched_barrier(0);
+        // s[b][r] is the raw score of key kb + 32 b + 8 (r / 4) + 4 fh + r % 4 for this lane's
+        // query.  Only the diagonal tile and the span's tail need the predicate; it is
+        // applied in one branch per tile.
+        if (kb + BKV - 1 > wq_lo || kb + BKV > n_kv) {
+            // key kq + off is allowed iff off <= lim (key <= qi and key < n_kv)
+            const int lim = min(qi, n_kv - 1) - (kb + 4 * fh);
 #pragma unroll
             for (int b = 0; b < 2; ++b)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    float v = s[b][r] * scale_log2;
-                    if (need_mask) {
-                        const int key = kb + b * 32 + 8 * (r >> 2) + 4 * fh + (r & 3);
-                        if (key > qi || key >= n_kv) v = -INFINITY;
-                    }
-                    s[b][r] = v;
-                    mx = fmaxf(mx, v);
-                }
-            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+                for (int r = 0; r < 16; ++r)
+                    if (32 * b + 8 * (r >> 2) + (r & 3) > lim) s[b][r] = -INFINITY;
+        }
+        // online softmax on raw scores.  m_i is a per-lane reference maximum, kept unscaled;
+        // the scale 1/sqrt(D) (in log2 units) is folded into one FMA per score before the
+        // hardware exp2, and masked scores (-inf) give exactly 0.  The reference moves only
+        // when a score exceeds it by more than kLazy (2^8 in probability), so probabilities
+        // stay <= 2^8 and the output accumulators are rescaled only on those rare steps.
+        float mx = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[b][r]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        if (__any(mx > m_i + lazy)) {
             const float m_new = fmaxf(m_i, mx);
-            const float corr = exp2f(m_i - m_new);
-            float rs = 0.f;
-#pragma unroll
-            for (int b = 0; b < 2; ++b)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float p = exp2f(s[b][r] - m_new);
-                    s[b][r] = p;
-                    rs += p;
-                }
-            rs += __shfl_xor(rs, 32, kWave);
-            l_i = l_i * corr + rs;
-            m_i = m_new;
+            const float corr = __builtin_amdgcn_exp2f((m_i - m_new) * scale_log2);
+            l_i *= corr;
 #pragma unroll
             for (int db = 0; db < HD / 32; ++db) o[db] *= corr;
+            m_i = m_new;
+        }
+        const float nm = -m_i * scale_log2;
+        float rs = 0.f;
 #pragma unroll
-            for (int sub = 0; sub < BKV / 16; ++sub) {
-                bf16x8 pf;
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(s[sub >> 1][(sub & 1) * 8 + e]);
-#pragma unroll
-                for (int db = 0; db < HD / 32; ++db) {
-                    s16x4 v2[2];
-#pragma unroll
-                    for (int r = 0; r < 2; ++r) {
-                        const int row = sub * 16 + 8 * r + vrow;
-                        const int d = db * 32 + vd;
-                        const char* p = stage + TILE_B + row * ROW + 16 * ((d >> 3) ^ vs) + (d & 7) * 2;
-                        v2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));   // generic -> LDS
-                    }
-                    const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
-                    o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[db], 0, 0, 0);
-                }
+            for (int r = 0; r < 16; ++r) {
+                const float p = __builtin_amdgcn_exp2f(fmaf(s[b][r], scale_log2, nm));
+                s[b][r] = p;
+                rs += p;
             }
+        rs += __shfl_xor(rs, 32, kWave);
+        l_i += rs;
+#pragma unroll
+        for (int sub = 0; sub < BKV / 16; ++sub) {
+            bf16x8 pf;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(s[sub >> 1][(sub & 1) * 8 + e]);
+#pragma unroll
+            for (int db = 0; db < HD / 32; ++db)
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[sub][db], pf, o[db], 0, 0, 0);
         }
     }
 
