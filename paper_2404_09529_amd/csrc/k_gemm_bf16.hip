@@ -40,6 +40,8 @@ constexpr int ROW_B = BK * 2;           // LDS row: 128 bytes = 8 chunks of 16 b
 constexpr int OP_B = BM * ROW_B;        // one operand tile in LDS (32 KB)
 constexpr int STAGE_B = 2 * OP_B;       // A tile then B tile (64 KB); two stages = 128 KB
 constexpr int LOADS = BM * ROW_B / 1024 / 4;  // 1 KB direct-to-LDS loads per wavefront per stage (8)
+// each stage request is LOADS loads plus one L2 prefetch; the vmcnt immediates below assume 9
+static_assert(LOADS + 1 == 9, "the vmcnt waits of the K loop assume 9 loads per stage request");
 constexpr int PF_DIST = 2;              // K steps between an L2 prefetch and the load it serves
 constexpr int PF_LDS = 2 * STAGE_B;     // 2 x 256 B of LDS that prefetches land in (never read)
 constexpr int LDS_BYTES = PF_LDS + 512;
@@ -210,7 +212,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
     }
     const int lds_op = load_b ? OP_B : 0;
     // L2 prefetch: wavefronts 0 and 4 each touch one 64-row quarter of their operand's K
-    // slice PF_DIST steps ahead, one 128-byte line (a row's 64 K values) per lane.
+    // slice PF_DIST steps ahead, one 128-byte line (a row's 64 K values) per lane; the other
+    // wavefronts issue the same instruction through an empty descriptor, so every wavefront
+    // has the same loads in flight and the same waits.
     const bool pf_wave = (wave & 3) == 0;
 
     // ---- wavefront sub-tile: 128 (N) x 64 (M) = 4 x 2 MFMA blocks of 32 x 32
@@ -249,20 +253,23 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
         // The tiles of a block that share an A panel have consecutive nt, those sharing a B
         // panel consecutive mt, so between them they prefetch every quarter once.
         const int pf_off = static_cast<int>(((load_b ? (mt & 3) : (nt & 3)) * 64 + lane) * ld * 2);
-        auto issue_loads = [&](int kt) {
+        // an empty descriptor: loads through it touch no memory and deposit zeros in LDS
+        const __amdgpu_buffer_rsrc_t rsrc_0 = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A), 0, 0, kRsrcWord3);
+        const __amdgpu_buffer_rsrc_t rsrc_pf = pf_wave ? rsrc : rsrc_0;
+        // LOADS loads of stage kt (through the empty descriptor when !live), then the prefetch
+        // (slice index clamped): every wavefront has exactly one younger load behind a stage
+        auto issue_loads = [&](int kt, bool live) {
             char* stage = smem + (kt & 1) * STAGE_B + lds_op;
+            const __amdgpu_buffer_rsrc_t r = live ? rsrc : rsrc_0;
 #pragma unroll
             for (int t = 0; t < LOADS; ++t) {
                 lds_void* dst = (lds_void*)(stage + ((wave & 3) * LOADS + t) * 1024);   // generic -> LDS
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[t], kt * BK * 2, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff[t], kt * BK * 2, 0, 0);
             }
-            if (pf_wave) {
-                // always issued (the slice index is clamped), so these wavefronts always have
-                // exactly one younger load outstanding behind a stage's loads
-                const int kp = min(kt + PF_DIST, nk - 1);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(smem + PF_LDS + (wave >> 2) * 256), 4,
-                                                         pf_off, kp * BK * 2, 0, 0);
-            }
+            const int kp = min(kt + PF_DIST, nk - 1);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(live ? rsrc_pf : rsrc_0,
+                                                     (lds_void*)(smem + PF_LDS + (wave >> 2) * 256), 4, pf_off,
+                                                     kp * BK * 2, 0, 0);
         };
 
         f32x16 acc[4][2];
@@ -302,36 +309,35 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
         // refilled only after both groups have read it.  Both groups execute 2 nk + 2
         // barriers, and every LDS read of the tile has completed before the last one, so the
         // next tile may refill either stage right after it.
-        issue_loads(0);
+        issue_loads(0, true);
         __builtin_amdgcn_s_waitcnt(0);
         barrier();
         if (grp == 0) {
             for (int kt = 0; kt < nk; ++kt) {
                 read_frags(kt);
-                if (kt + 1 < nk) issue_loads(kt + 1);        // after the LDS reads: they start first
+                if (kt + 1 < nk) issue_loads(kt + 1, true);    // after the LDS reads: they start first
                 __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
                 barrier();
                 mfmas();
-                // this group's part of tile kt+1: vmcnt(0), or vmcnt(1) behind the prefetch
-                if (pf_wave) __builtin_amdgcn_s_waitcnt(0x0f71);
-                else __builtin_amdgcn_s_waitcnt(0x0f70);
+                __builtin_amdgcn_s_waitcnt(0x0f71);          // vmcnt(1): this group's part of tile kt+1
                 barrier();
             }
             barrier();
         } else {
-            if (nk > 1) issue_loads(1);
+            issue_loads(1, nk > 1);
             barrier();
             for (int kt = 0; kt < nk; ++kt) {
                 read_frags(kt);
-                // fragments, and this group's part of tile kt+1 (vmcnt(1) behind the prefetch)
-                if (pf_wave) __builtin_amdgcn_s_waitcnt(0x0071);
-                else __builtin_amdgcn_s_waitcnt(0x0070);
+                // Tile kt+2 goes to the stage this group has just finished reading (group 0 read
+                // it in phase 2kt), so its loads are issued here, in this group's memory phase:
+                // group 0 issues its loads in the other phase, and the CU's single address unit
+                // then sees half of a K step's loads in each phase.  They are waited for one
+                // iteration later, so they have two phases to land.
+                __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
+                issue_loads(kt + 2, kt + 2 < nk);
+                __builtin_amdgcn_s_waitcnt(0x0f79);          // vmcnt(9): tile kt+1 landed, kt+2 in flight
                 barrier();
                 mfmas();
-                // issued after the MFMA burst so the load issue does not delay it; tile kt+2
-                // goes to the stage both groups finished reading in phases 2kt and 2kt+1, and
-                // is waited for at the end of this group's next memory phase (phase 2kt+3)
-                if (kt + 2 < nk) issue_loads(kt + 2);
                 barrier();
             }
         }
