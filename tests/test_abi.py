@@ -220,3 +220,18 @@ def test_step_entry_points_reject_before_enqueue(L):
     # a prompt too long for the kernel's 32-bit cache addressing is refused up front
     huge = _dplan(capacity=1100000, n_rows=1, max_len=1100000, total_len=300)   # x 8 KV heads x 256 B > 2 GiB
     assert a(ctypes.byref(cfg), ctypes.byref(huge), 0x1000, 4096, 1, 1, 1, None) == pp.PP_ERR_UNSUPPORTED
+
+
+def test_gemm_rejects_unsupported_shapes_before_enqueue(L):
+    """bf16 GEMM tiling limits are checked on the host (no launch, no GPU needed)."""
+    g = L.pp_gemm
+    ok = dict(A=0x1000, lda=4096, B=0x2000, ldb=4096, C=0x3000, ldc=4096, M=256, N=4096, K=4096)
+    def call(**kw):
+        a = {**ok, **kw}
+        return g(pp.PP_BF16, pp.PP_EPI_STORE, a["A"], a["lda"], a["B"], a["ldb"], a["C"], a["ldc"], a["M"], a["N"],
+                 a["K"], None, None)
+    assert call(N=4000) == pp.PP_ERR_UNSUPPORTED          # N % 256
+    assert call(K=4000, lda=4000, ldb=4000) == pp.PP_ERR_UNSUPPORTED   # K % 64
+    assert call(lda=100) == pp.PP_ERR_INVALID_ARG          # lda < K
+    assert call(M=0) == pp.PP_OK                           # empty: nothing to do
+    assert g(pp.PP_BF16, 7, 0x1000, 4096, 0x2000, 4096, 0x3000, 4096, 256, 4096, 4096, None, None) == pp.PP_ERR_INVALID_ARG
