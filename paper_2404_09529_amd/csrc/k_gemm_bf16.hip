@@ -25,8 +25,8 @@
 // round-robin, so XCD x runs workgroups x, x + 8, ...; each XCD owns a contiguous block of
 // M-tiles ordered in groups of up to 8 M-tiles sweeping N, and its workgroups take that list
 // in strides of their count, so the 32 tiles resident on an XCD always form one compact
-// block started together.  Each tile also prefetches a quarter of its next K slices into L2
-// (the sharers of a panel pick different quarters), so most LDS fills hit L2.  M-tiles made
+// block started together, and the tiles sharing an A or B panel read it from the same L2.
+// M-tiles made
 // only of row-tail padding are skipped (packed batches only carry pads at row tails,
 // section 3.1).
 #include "device.h"
@@ -40,11 +40,9 @@ constexpr int ROW_B = BK * 2;           // LDS row: 128 bytes = 8 chunks of 16 b
 constexpr int OP_B = BM * ROW_B;        // one operand tile in LDS (32 KB)
 constexpr int STAGE_B = 2 * OP_B;       // A tile then B tile (64 KB); two stages = 128 KB
 constexpr int LOADS = BM * ROW_B / 1024 / 4;  // 1 KB direct-to-LDS loads per wavefront per stage (8)
-// each stage request is LOADS loads plus one L2 prefetch; the vmcnt immediates below assume 9
-static_assert(LOADS + 1 == 9, "the vmcnt waits of the K loop assume 9 loads per stage request");
-constexpr int PF_DIST = 2;              // K steps between an L2 prefetch and the load it serves
-constexpr int PF_LDS = 2 * STAGE_B;     // 2 x 256 B of LDS that prefetches land in (never read)
-constexpr int LDS_BYTES = PF_LDS + 512;
+// group 1 waits for one stage with the next stage's LOADS loads still in flight (vmcnt(8))
+static_assert(LOADS == 8, "the vmcnt waits of the K loop assume 8 loads per stage request");
+constexpr int LDS_BYTES = 2 * STAGE_B;
 // Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
 constexpr int kRsrcWord3 = 0x00020000;
 
@@ -211,11 +209,6 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
         voff[t] = static_cast<int>(row * ld * 2) + 16 * ((lane & 7) ^ swz(row));
     }
     const int lds_op = load_b ? OP_B : 0;
-    // L2 prefetch: wavefronts 0 and 4 each touch one 64-row quarter of their operand's K
-    // slice PF_DIST steps ahead, one 128-byte line (a row's 64 K values) per lane; the other
-    // wavefronts issue the same instruction through an empty descriptor, so every wavefront
-    // has the same loads in flight and the same waits.
-    const bool pf_wave = (wave & 3) == 0;
 
     // ---- wavefront sub-tile: 128 (N) x 64 (M) = 4 x 2 MFMA blocks of 32 x 32
     const int wn = wave & 1, wm = wave >> 1;
@@ -250,26 +243,13 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
                                                 static_cast<int>(BN * ldb * 2), kRsrcWord3)
             : __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A + int64_t(m0) * lda), 0,
                                                 static_cast<int>(a_rows * lda * 2), kRsrcWord3);
-        // The tiles of a block that share an A panel have consecutive nt, those sharing a B
-        // panel consecutive mt, so between them they prefetch every quarter once.
-        const int pf_off = static_cast<int>(((load_b ? (mt & 3) : (nt & 3)) * 64 + lane) * ld * 2);
-        // an empty descriptor: loads through it touch no memory and deposit zeros in LDS
-        const __amdgpu_buffer_rsrc_t rsrc_0 = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A), 0, 0, kRsrcWord3);
-        const __amdgpu_buffer_rsrc_t rsrc_pf = pf_wave ? rsrc : rsrc_0;
-        // LOADS loads of stage kt (through the empty descriptor when !live), then the prefetch
-        // (slice index clamped): every wavefront has exactly one younger load behind a stage
-        auto issue_loads = [&](int kt, bool live) {
+        auto issue_loads = [&](int kt) {
             char* stage = smem + (kt & 1) * STAGE_B + lds_op;
-            const __amdgpu_buffer_rsrc_t r = live ? rsrc : rsrc_0;
 #pragma unroll
             for (int t = 0; t < LOADS; ++t) {
                 lds_void* dst = (lds_void*)(stage + ((wave & 3) * LOADS + t) * 1024);   // generic -> LDS
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff[t], kt * BK * 2, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[t], kt * BK * 2, 0, 0);
             }
-            const int kp = min(kt + PF_DIST, nk - 1);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(live ? rsrc_pf : rsrc_0,
-                                                     (lds_void*)(smem + PF_LDS + (wave >> 2) * 256), 4, pf_off,
-                                                     kp * BK * 2, 0, 0);
         };
 
         f32x16 acc[4][2];
@@ -309,22 +289,25 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
         // refilled only after both groups have read it.  Both groups execute 2 nk + 2
         // barriers, and every LDS read of the tile has completed before the last one, so the
         // next tile may refill either stage right after it.
-        issue_loads(0, true);
+        // Waits never rely on loads retiring in issue order across descriptors: group 0's A
+        // loads (rows past M read as zero) are waited for with vmcnt(0); group 1's B loads
+        // are all in range, and it keeps only the next stage's LOADS loads in flight.
+        issue_loads(0);
         __builtin_amdgcn_s_waitcnt(0);
         barrier();
         if (grp == 0) {
             for (int kt = 0; kt < nk; ++kt) {
                 read_frags(kt);
-                if (kt + 1 < nk) issue_loads(kt + 1, true);    // after the LDS reads: they start first
+                if (kt + 1 < nk) issue_loads(kt + 1);        // after the LDS reads: they start first
                 __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
                 barrier();
                 mfmas();
-                __builtin_amdgcn_s_waitcnt(0x0f71);          // vmcnt(1): this group's part of tile kt+1
+                __builtin_amdgcn_s_waitcnt(0x0f70);          // vmcnt(0): this group's part of tile kt+1
                 barrier();
             }
             barrier();
         } else {
-            issue_loads(1, nk > 1);
+            if (nk > 1) issue_loads(1);
             barrier();
             for (int kt = 0; kt < nk; ++kt) {
                 read_frags(kt);
@@ -334,8 +317,12 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
                 // then sees half of a K step's loads in each phase.  They are waited for one
                 // iteration later, so they have two phases to land.
                 __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
-                issue_loads(kt + 2, kt + 2 < nk);
-                __builtin_amdgcn_s_waitcnt(0x0f79);          // vmcnt(9): tile kt+1 landed, kt+2 in flight
+                if (kt + 2 < nk) {
+                    issue_loads(kt + 2);
+                    __builtin_amdgcn_s_waitcnt(0x0f78);      // vmcnt(8): tile kt+1 landed, kt+2 in flight
+                } else {
+                    __builtin_amdgcn_s_waitcnt(0x0f70);      // vmcnt(0)
+                }
                 barrier();
                 mfmas();
                 barrier();
@@ -343,7 +330,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
         }
         epilogue<EPI>(acc, Cv, ldc, M, m0, n0, wm, wn, fr, fh, slot_seg, qo);
     }
-    __builtin_amdgcn_s_waitcnt(0);   // no prefetch may still be writing LDS when the workgroup ends
+    __builtin_amdgcn_s_waitcnt(0);   // no load may still be writing LDS when the workgroup ends
 }
 
 }  // namespace
