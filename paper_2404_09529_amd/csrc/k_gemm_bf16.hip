@@ -4,17 +4,23 @@
 // C[M, N] = A[M, K] B[N, K]^T with A the packed activations (bf16, K contiguous) and B a
 // weight matrix in [out, in] layout (bf16, K contiguous), float32 accumulation.
 //
-// Tiling: one 512-thread workgroup (8 wavefronts) per 256 x 256 output tile, K consumed in
-// steps of 64.  Each wavefront owns a 128 (N) x 64 (M) sub-tile = 4 x 2 blocks of the
-// 32x32x16 bf16 MFMA, 128 accumulator registers.  The weight block is the MFMA's first
-// operand, so a lane's accumulators are 4-element runs along N of one activation row:
-// the epilogue writes 8-byte (bf16) or 16-byte (float32) runs without a transpose.
+// Tiling: one 256-thread workgroup (4 wavefronts, one per SIMD) per 256 x 256 output tile,
+// K consumed in steps of 64.  Each wavefront owns a 128 (N) x 128 (M) sub-tile = 4 x 4
+// blocks of the 32x32x16 bf16 MFMA; its 256 float32 accumulators live in the accumulation
+// registers.  The weight block is the MFMA's first operand, so a lane's accumulators are
+// 4-element runs along N of one activation row: the epilogue writes 8-byte (bf16) or
+// 16-byte (float32) runs without a transpose.
 //
-// Data path: tiles go straight from global memory into LDS (buffer loads with the LDS
-// destination, no staging registers), double-buffered (2 x 64 KB).  Eight wavefronts, two
-// per SIMD, run a ping-pong schedule: while one wavefront of a SIMD reads a whole K step of
-// MFMA fragments from LDS, the other issues its 32 MFMAs back to back, and they swap at
-// every barrier.
+// Data path: operand tiles go straight from global memory into LDS (buffer loads with the
+// LDS destination, no staging registers), whole 128-byte row segments per request.  The LDS
+// is a ring of 5 slots of 32 KB, each holding one operand (A or B) of one K-step; slots are
+// filled in the order A0 B0 A1 B1 ... and freed in pairs when a step has been read, so the
+// A tile of step g+2 is already loading while step g is consumed.  The workgroup's tiles
+// form one continuous stream of K-steps: the loads cross tile boundaries, and the first
+// steps of the next tile land while the epilogue of the current one runs.  A step is four
+// sub-steps of 16 MFMAs per wavefront; each sub-step also reads the MFMA fragments of the
+// next sub-step from LDS and issues a quarter of an operand tile (4 loads per wavefront),
+// which keeps the CU's address unit about half busy at all times.  One barrier per step.
 //
 // Epilogues: bf16 store; float32 residual add; SwiGLU over interleaved gate/up blocks; and,
 // for the QKV projection, RoPE at the restart positions (section 3.2) applied to the float32
@@ -25,8 +31,7 @@
 // round-robin, so XCD x runs workgroups x, x + 8, ...; each XCD owns a contiguous block of
 // M-tiles ordered in groups of up to 8 M-tiles sweeping N, and its workgroups take that list
 // in strides of their count, so the 32 tiles resident on an XCD always form one compact
-// block started together, and the tiles sharing an A or B panel read it from the same L2.
-// M-tiles made
+// block, and the tiles sharing an A or B panel read it from the same L2.  M-tiles made
 // only of row-tail padding are skipped (packed batches only carry pads at row tails,
 // section 3.1).
 #include "device.h"
@@ -35,14 +40,17 @@
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int NT = 512;                 // 8 wavefronts, 2 per SIMD
-constexpr int ROW_B = BK * 2;           // LDS row: 128 bytes = 8 chunks of 16 bytes
-constexpr int OP_B = BM * ROW_B;        // one operand tile in LDS (32 KB)
-constexpr int STAGE_B = 2 * OP_B;       // A tile then B tile (64 KB); two stages = 128 KB
-constexpr int LOADS = BM * ROW_B / 1024 / 4;  // 1 KB direct-to-LDS loads per wavefront per stage (8)
-// group 1 waits for one stage with the next stage's LOADS loads still in flight (vmcnt(8))
-static_assert(LOADS == 8, "the vmcnt waits of the K loop assume 8 loads per stage request");
-constexpr int LDS_BYTES = 2 * STAGE_B;
+constexpr int NT = 256;                  // 4 wavefronts, one per SIMD
+constexpr int ROW_B = BK * 2;            // LDS row: 128 bytes = 8 chunks of 16 bytes
+constexpr int SLOT_B = BM * ROW_B;       // one operand of one K-step (32 KB)
+constexpr int NSLOT = 5;                 // the whole 160 KB LDS of a CU
+constexpr int LDS_BYTES = NSLOT * SLOT_B;
+constexpr int QUARTER = SLOT_B / 1024 / 4 / 2;   // 1 KB loads per wavefront per quarter operand (4)
+static_assert(QUARTER == 4, "the vmcnt wait of the K loop counts 8 loads per operand tile");
+
+// s_waitcnt immediate: vmcnt(n) and lgkmcnt(0), expcnt not waited for (gfx9 encoding:
+// vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
+constexpr int wait_vm_lgkm0(int n) { return ((n >> 4) << 14) | (n & 15) | 0x0070; }
 // Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
 constexpr int kRsrcWord3 = 0x00020000;
 
@@ -66,33 +74,75 @@ __device__ __forceinline__ void barrier() {
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// Epilogue of one tile: the lane holds, for activation rows m (two, one per j), runs of 4
-// consecutive n of four 32-column blocks.
+// The accumulators of activation block j, pinned in the accumulation registers at this point:
+// the epilogue then moves them to vector registers one block at a time instead of all at once
+// (which would need every vector register and spill).  The accumulators are dead afterwards.
+__device__ __forceinline__ void take_block(f32x16 (&acc)[4][4], int j, f32x16 (&c)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        asm volatile("" : "+a"(acc[i][j]) : : "memory");
+        c[i] = acc[i][j];
+    }
+}
+
+// Staged bf16 output of one activation block: 32 rows x `cols` bf16 written by the lanes in
+// MFMA layout to this wavefront's LDS staging area, then read back as whole 16-byte chunks of
+// rows and stored with each instruction covering complete rows (full cache lines).  Row r's
+// 16-byte chunk c sits at chunk c ^ (r % chunks) of the staging row.
+template <int CHUNKS>
+__device__ __forceinline__ void stage_put(char* stg, int r, int c, int fh, bf16x4 v) {
+    *reinterpret_cast<bf16x4*>(stg + r * CHUNKS * 16 + ((c ^ (r % CHUNKS)) * 16) + fh * 8) = v;
+}
+
+// The epilogue of one wavefront sub-tile (activation rows mb.., weight rows nb0..): the lane
+// holds, for activation rows m (four, one per j), runs of 4 consecutive n of four 32-column
+// blocks.  stg is this wavefront's 8 KB of LDS, free for the duration of the epilogue.
 template <int EPI>
-__device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], void* __restrict__ Cv, int64_t ldc, int M,
-                                         int m0, int n0, int wm, int wn, int fr, int fh,
-                                         const int32_t* __restrict__ slot_seg, const ppk::QkvOut& qo) {
+__device__ __forceinline__ void epilogue(f32x16 (&acc)[4][4], void* __restrict__ Cv, int64_t ldc, int M,
+                                         int mb, int nb0, int lane, const int32_t* __restrict__ slot_seg,
+                                         const ppk::QkvOut& qo, char* stg) {
+    const int fr = lane & 31, fh = lane >> 5;
+    if constexpr (EPI == ppk::kResidual) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f32x16 cj[4];
+            take_block(acc, j, cj);
+            const int m = mb + j * 32 + fr;
+            if (m >= M) continue;
+            float* C = static_cast<float*>(Cv) + int64_t(m) * ldc + nb0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    f32x4* p = reinterpret_cast<f32x4*>(C + i * 32 + q * 8 + fh * 4);
+                    f32x4 v = *p;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] += cj[i][q * 4 + e];
+                    *p = v;
+                }
+        }
+        return;
+    }
+    // bf16 outputs: 128 columns (16 chunks) per row, or 64 (8 chunks) after SwiGLU
+    constexpr int CH = EPI == ppk::kSwiGLU ? 8 : 16;
+    int head = 0, kind = 0;
     if constexpr (EPI == ppk::kQkvRope) {
         // The wavefront's 128 columns are exactly one head (tiles start at multiples of 256),
         // and the rotate-half partners c and c + 64 are accumulator blocks i and i + 2 of the
         // same lane: RoPE is applied to the float32 accumulators before the one rounding.
-        const int head = (n0 + wn * 128) >> 7;
-        const int kind = head < qo.H ? 0 : (head < qo.H + qo.Hkv ? 1 : 2);   // q, k, v (uniform)
+        head = nb0 >> 7;
+        kind = head < qo.H ? 0 : (head < qo.H + qo.Hkv ? 1 : 2);   // q, k, v (uniform)
+    }
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int m = m0 + wm * 64 + j * 32 + fr;
-            if (m >= M) continue;
-            bf16* dst;
-            if (kind == 0) {
-                dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
-            } else {
-                const int kv = qo.slot_kv[m];
-                if (kv < 0) continue;
-                dst = static_cast<bf16*>(kind == 1 ? qo.kc : qo.vc) + int64_t(kv) * qo.ldkv +
-                      (head - qo.H - (kind == 2 ? qo.Hkv : 0)) * 128;
-            }
+    for (int j = 0; j < 4; ++j) {
+        f32x16 c[4];
+        take_block(acc, j, c);
+        const int m = mb + j * 32 + fr;
+        int dst_row = m;   // row of the destination that activation row m goes to (< 0: none)
+        if constexpr (EPI == ppk::kQkvRope) {
+            if (kind > 0) dst_row = m < M ? qo.slot_kv[m] : -1;
             if (kind < 2) {
-                const int pos = slot_seg[m] >= 0 ? qo.slot_pos[m] : 0;
+                const int pos = m < M && slot_seg[m] >= 0 ? qo.slot_pos[m] : 0;
                 const float2* cs = qo.table + int64_t(pos) * 64 + fh * 4;
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
@@ -105,75 +155,74 @@ __device__ __forceinline__ void epilogue(const f32x16 (&acc)[4][2], void* __rest
                         bf16x4 lo, hi;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            const float a = acc[i][j][q * 4 + e], b = acc[i + 2][j][q * 4 + e];
+                            const float a = c[i][q * 4 + e], b = c[i + 2][q * 4 + e];
                             lo[e] = static_cast<bf16>(a * cv[e] - b * sv[e]);
                             hi[e] = static_cast<bf16>(b * cv[e] + a * sv[e]);
                         }
-                        *reinterpret_cast<bf16x4*>(dst + i * 32 + q * 8 + fh * 4) = lo;
-                        *reinterpret_cast<bf16x4*>(dst + 64 + i * 32 + q * 8 + fh * 4) = hi;
-                    }
-            } else {
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        bf16x4 v;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(acc[i][j][q * 4 + e]);
-                        *reinterpret_cast<bf16x4*>(dst + i * 32 + q * 8 + fh * 4) = v;
+                        stage_put<CH>(stg, fr, i * 4 + q, fh, lo);
+                        stage_put<CH>(stg, fr, 8 + i * 4 + q, fh, hi);
                     }
             }
         }
-        return;
-    }
+        if constexpr (EPI == ppk::kSwiGLU) {
+            // rows 32 i .. +15 of block i are gate rows, 32 i + 16 .. +31 the matching up rows:
+            // output column 16 i + 8 q + 4 fh + e
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int m = m0 + wm * 64 + j * 32 + fr;
-        if (m >= M) continue;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int nb = n0 + wn * 128 + i * 32;
-            const f32x16& c = acc[i][j];
-            if constexpr (EPI == ppk::kStore) {
-                bf16* C = static_cast<bf16*>(Cv) + int64_t(m) * ldc;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    bf16x4 v;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(c[q * 4 + e]);
-                    *reinterpret_cast<bf16x4*>(C + nb + q * 8 + fh * 4) = v;
-                }
-            } else if constexpr (EPI == ppk::kResidual) {
-                float* C = static_cast<float*>(Cv) + int64_t(m) * ldc;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    f32x4* p = reinterpret_cast<f32x4*>(C + nb + q * 8 + fh * 4);
-                    f32x4 v = *p;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] += c[q * 4 + e];
-                    *p = v;
-                }
-            } else {
-                // rows nb..nb+15 of this block are gate rows, nb+16..nb+31 the matching up rows
-                bf16* C = static_cast<bf16*>(Cv) + int64_t(m) * ldc + nb / 2;
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int q = 0; q < 2; ++q) {
                     bf16x4 v;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(silu(c[q * 4 + e]) * c[(q + 2) * 4 + e]);
-                    *reinterpret_cast<bf16x4*>(C + q * 8 + fh * 4) = v;
+                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(silu_rcp(c[i][q * 4 + e]) * c[i][(q + 2) * 4 + e]);
+                    stage_put<CH>(stg, fr, i * 2 + q, fh, v);
                 }
+        } else if (EPI == ppk::kStore || kind == 2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    bf16x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(c[i][q * 4 + e]);
+                    stage_put<CH>(stg, fr, i * 4 + q, fh, v);
+                }
+        }
+        // read back whole rows: instruction k covers rows (64 / CH) k .. of the block
+        constexpr int RPI = 64 / CH;   // rows per instruction
+        bf16x8 v[32 / RPI];
+#pragma unroll
+        for (int k = 0; k < 32 / RPI; ++k) {
+            const int r = k * RPI + lane / CH, ch = lane % CH;
+            v[k] = *reinterpret_cast<const bf16x8*>(stg + r * CH * 16 + ((ch ^ (r % CH)) * 16));
+        }
+#pragma unroll
+        for (int k = 0; k < 32 / RPI; ++k) {
+            const int r = k * RPI + lane / CH, ch = lane % CH;
+            const int mr = mb + j * 32 + r;
+            if constexpr (EPI == ppk::kQkvRope) {
+                const int drow = __shfl(dst_row, r);   // lane r holds row r's destination
+                if (mr >= M || drow < 0) continue;
+                bf16* dst = kind == 0 ? static_cast<bf16*>(qo.q) + int64_t(drow) * qo.ldq + head * 128
+                                      : static_cast<bf16*>(kind == 1 ? qo.kc : qo.vc) + int64_t(drow) * qo.ldkv +
+                                            (head - qo.H - (kind == 2 ? qo.Hkv : 0)) * 128;
+                *reinterpret_cast<bf16x8*>(dst + ch * 8) = v[k];
+            } else {
+                if (mr >= M) continue;
+                bf16* C = static_cast<bf16*>(Cv) + int64_t(mr) * ldc + (EPI == ppk::kSwiGLU ? nb0 / 2 : nb0);
+                *reinterpret_cast<bf16x8*>(C + ch * 8) = v[k];
             }
         }
     }
+    // the staging area is refilled by this wavefront's own loads right after the epilogue
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
 }
 
 template <int EPI>
-__global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ A, int64_t lda,
-                                                       const bf16* __restrict__ B, int64_t ldb,
-                                                       void* __restrict__ Cv, int64_t ldc, int M, int K,
-                                                       const int32_t* __restrict__ slot_seg, int capacity,
-                                                       int tiles_m, int tiles_n, ppk::QkvOut qo) {
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict__ A, int64_t lda,
+                                                          const bf16* __restrict__ B, int64_t ldb,
+                                                          void* __restrict__ Cv, int64_t ldc, int M, int K,
+                                                          const int32_t* __restrict__ slot_seg, int capacity,
+                                                          int tiles_m, int tiles_n, ppk::QkvOut qo) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
@@ -184,8 +233,8 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
     // at most 8 M-tiles, each group sweeping all N-tiles; its workgroups take that list in
     // strides of their count.  The tiles resident on an XCD at any time are therefore one
     // compact block of the list (about 8 M x 4 N tiles) started together, at the same K step:
-    // each 64-wide K slice of an activation or weight panel is fetched into the XCD's L2 once
-    // and read there by every tile of the block.  Every XCD sweeps N at the same rate, so the
+    // each K slice of an activation or weight panel is fetched into the XCD's L2 once and
+    // read there by every tile of the block.  Every XCD sweeps N at the same rate, so the
     // weight panels are also shared through the last-level cache.
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, n_slots = gridDim.x >> 3;
     const int pm = (tiles_m + 7) / 8;
@@ -193,142 +242,183 @@ __global__ __launch_bounds__(NT) void gemm_bf16_kernel(const bf16* __restrict__ 
     if (m_cnt <= 0) return;
     const int n_groups = (m_cnt + 7) / 8, gm = (m_cnt + n_groups - 1) / n_groups;
     const int n_local = m_cnt * tiles_n;
+    auto tile_m0 = [&](int local) {
+        const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
+        const int first = group * gm, gsz = min(m_cnt - first, gm);
+        return (m_begin + first + within % gsz) * BM;
+    };
+    auto tile_n0 = [&](int local) {
+        const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
+        const int first = group * gm, gsz = min(m_cnt - first, gm);
+        return (within / gsz) * BN;
+    };
+    // the first tile of this workgroup's list at or after `local` that holds a real slot
+    auto next_active = [&](int local) {
+        for (; local < n_local; local += n_slots)
+            if (tile_active(slot_seg, capacity, tile_m0(local), M)) break;
+        return local;
+    };
+    const int nk = K / BK;
 
-    // ---- direct global -> LDS loads.  A stage holds the A tile then the B tile, 8 chunks of
-    // 16 bytes per row.  Load t of wavefront w fills 1 KB = rows 8 j .. 8 j + 7 of its operand
-    // (j = (w % 4) * 8 + t; wavefronts 0-3 load A, 4-7 load B); lane l lands at physical chunk
-    // l % 8 of row 8 j + l / 8, so it fetches the logical chunk that the swizzle puts there.
-    // Every quad of lanes reads one aligned 64-byte half of a row.  Rows of A past M read as
-    // zero (the descriptor ends at row min(M, m0 + 256)); every access is inside its buffer.
-    const bool load_b = wave >= 4;
-    const int64_t ld = load_b ? ldb : lda;
-    int voff[LOADS];
+    // ---- direct global -> LDS loads.  Load t (0..7) of wavefront w fills 1 KB = rows
+    // 64 w + 8 t .. + 7 of an operand tile; lane l lands at physical chunk l % 8 of row
+    // 64 w + 8 t + l / 8 and fetches the logical chunk that the swizzle puts there
+    // (f = (l / 8) ^ t for these rows).  Rows of A past M are read as row M - 1: every load is
+    // in range, so loads complete in the order they were issued, and the results of the
+    // duplicated rows are never stored.
+    const int64_t lda2 = lda * 2, ldb2 = ldb * 2;
+    const int lrow = lane >> 3;
+    int chunk_off[2 * QUARTER], voff_b[2 * QUARTER], voff_a[2 * QUARTER];
 #pragma unroll
-    for (int t = 0; t < LOADS; ++t) {
-        const int row = 8 * ((wave & 3) * LOADS + t) + lane / 8;
-        voff[t] = static_cast<int>(row * ld * 2) + 16 * ((lane & 7) ^ swz(row));
+    for (int t = 0; t < 2 * QUARTER; ++t) {
+        chunk_off[t] = 16 * ((lane & 7) ^ lrow ^ t);
+        voff_b[t] = static_cast<int>((64 * wave + 8 * t + lrow) * ldb2) + chunk_off[t];
     }
-    const int lds_op = load_b ? OP_B : 0;
 
-    // ---- wavefront sub-tile: 128 (N) x 64 (M) = 4 x 2 MFMA blocks of 32 x 32
+    // load cursor: the K-step whose operand tiles are being requested, in slots l_sa (A) and
+    // l_sb (B); l_local >= n_local once the stream is exhausted (its loads are then dead:
+    // they read nothing and land in slots that are never read again)
+    int l_local = next_active(slot), l_kt = 0, l_sa = 0, l_sb = 1;
+    __amdgpu_buffer_rsrc_t rsrc_a, rsrc_b;
+    const __amdgpu_buffer_rsrc_t rsrc_0 = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A), 0, 0, kRsrcWord3);
+    auto set_cursor_tile = [&]() {
+        if (l_local < n_local) {
+            const int m0 = tile_m0(l_local), n0 = tile_n0(l_local);
+            const int a_rows = min(M - m0, BM);
+            rsrc_a = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A + int64_t(m0) * lda), 0,
+                                                       static_cast<int>(a_rows * lda2), kRsrcWord3);
+            rsrc_b = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(B + int64_t(n0) * ldb), 0,
+                                                       static_cast<int>(BN * ldb2), kRsrcWord3);
+#pragma unroll
+            for (int t = 0; t < 2 * QUARTER; ++t)
+                voff_a[t] = static_cast<int>(min(64 * wave + 8 * t + lrow, a_rows - 1) * lda2) + chunk_off[t];
+        } else {
+            rsrc_a = rsrc_0;
+            rsrc_b = rsrc_0;
+        }
+    };
+    set_cursor_tile();
+    auto load_a = [&](int t) {
+        char* dst = smem + l_sa * SLOT_B + (wave * 2 * QUARTER + t) * 1024;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_a, (lds_void*)dst, 16, voff_a[t], l_kt * BK * 2, 0, 0);
+    };
+    auto load_b = [&](int t) {
+        char* dst = smem + l_sb * SLOT_B + (wave * 2 * QUARTER + t) * 1024;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_b, (lds_void*)dst, 16, voff_b[t], l_kt * BK * 2, 0, 0);
+    };
+    auto advance_cursor = [&]() {
+        l_sa = l_sa >= NSLOT - 2 ? l_sa + 2 - NSLOT : l_sa + 2;
+        l_sb = l_sb >= NSLOT - 2 ? l_sb + 2 - NSLOT : l_sb + 2;
+        if (l_local >= n_local) return;
+        if (++l_kt == nk) {
+            l_kt = 0;
+            l_local = next_active(l_local + n_slots);
+            set_cursor_tile();
+        }
+    };
+
+    // ---- wavefront sub-tile: 128 (N) x 128 (M) = 4 x 4 MFMA blocks of 32 x 32
     const int wn = wave & 1, wm = wave >> 1;
-    const int grp = wave >> 2;               // waves w and w + 4 share a SIMD
     const int fr = lane & 31, fh = lane >> 5;
-
     // fragment addresses.  Row r = base + 32 i + fr of either operand has swizzle
-    // f(r) = g ^ 4 (i & 1) with g = ((fr & 7) ^ (fr >> 3)) & 7 (base is a multiple of 64), so
+    // f(r) = g ^ 4 (i & 1) with g = ((fr & 7) ^ (fr >> 3)) & 7 (base is a multiple of 128), so
     // the physical chunk of logical chunk 2 ks + fh is (2 (ks ^ 2 (i & 1))) ^ (fh ^ g): four
     // per-lane offsets cover every (ks, i); the block stride (32 rows = 4 KB) is immediate.
-    const int gsw = ((fr & 7) ^ (fr >> 3)) & 7;
-    const int x = fh ^ gsw;
+    const int x = fh ^ (((fr & 7) ^ (fr >> 3)) & 7);
     int a_lds[4], b_lds[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
-        a_lds[m] = (wm * 64 + fr) * ROW_B + 16 * ((2 * m) ^ x);
-        b_lds[m] = OP_B + (wn * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
+        a_lds[m] = (wm * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
+        b_lds[m] = (wn * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
     }
-    const int nk = K / BK;
+    struct Frags { bf16x8 w[4], a[4]; };
+    // fragment q of sub-step ks of the step held in slots (sa, sb), in the order the MFMAs
+    // first need them: w0, a0..a3, w1..w3
+    auto read_one = [&](int sa, int sb, int ks, int q, Frags& f) {
+        if (q == 0) {
+            f.w[0] = *reinterpret_cast<const bf16x8*>(smem + sb * SLOT_B + b_lds[ks]);
+        } else if (q < 5) {
+            const int j = q - 1;
+            f.a[j] = *reinterpret_cast<const bf16x8*>(smem + sa * SLOT_B + a_lds[ks ^ (2 * (j & 1))] + j * 32 * ROW_B);
+        } else {
+            const int i = q - 4;
+            f.w[i] = *reinterpret_cast<const bf16x8*>(smem + sb * SLOT_B + b_lds[ks ^ (2 * (i & 1))] + i * 32 * ROW_B);
+        }
+    };
 
-    for (int local = slot; local < n_local; local += n_slots) {
-        const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
-        const int first = group * gm, gsz = min(m_cnt - first, gm);
-        const int mt = m_begin + first + within % gsz;
-        const int nt = within / gsz;
-        const int m0 = mt * BM, n0 = nt * BN;
-        if (!tile_active(slot_seg, capacity, m0, M)) continue;
-
-        const int a_rows = min(M - m0, BM);
-        const __amdgpu_buffer_rsrc_t rsrc = load_b
-            ? __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(B + int64_t(n0) * ldb), 0,
-                                                static_cast<int>(BN * ldb * 2), kRsrcWord3)
-            : __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A + int64_t(m0) * lda), 0,
-                                                static_cast<int>(a_rows * lda * 2), kRsrcWord3);
-        auto issue_loads = [&](int kt) {
-            char* stage = smem + (kt & 1) * STAGE_B + lds_op;
+    // ---- the K-step stream.  Step g holds slots 2g % 5 (A) and (2g+1) % 5 (B).  Per step:
+    //   sub-step 0: MFMAs (g, 0); read (g, 1); B tile of step g+1, loads 4-7
+    //   sub-step 1: MFMAs (g, 1); read (g, 2); A tile of step g+2, loads 0-3
+    //   sub-step 2: MFMAs (g, 2); read (g, 3); A tile of step g+2, loads 4-7
+    //   wait until step g+1 has landed and this wavefront's reads of step g are done; barrier
+    //   sub-step 3: MFMAs (g, 3); read (g+1, 0); B tile of step g+2, loads 0-3
+    // The slots of step g are free after the barrier; the B tile of g+2 is the first load to
+    // reuse one of them.  At the barrier the only loads issued after step g+1's are the 8 of
+    // the A tile of g+2, so vmcnt(8) (vmcnt(0) when g+2 does not exist) waits for g+1 exactly.
+    int c_local = l_local;
+    if (c_local >= n_local) return;
+    // prologue: steps 0 (A, B) and 1 (A, B loads 0-3)
 #pragma unroll
-            for (int t = 0; t < LOADS; ++t) {
-                lds_void* dst = (lds_void*)(stage + ((wave & 3) * LOADS + t) * 1024);   // generic -> LDS
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[t], kt * BK * 2, 0, 0);
-            }
-        };
-
-        f32x16 acc[4][2];
+    for (int t = 0; t < 2 * QUARTER; ++t) load_a(t);
+#pragma unroll
+    for (int t = 0; t < 2 * QUARTER; ++t) load_b(t);
+    advance_cursor();
+#pragma unroll
+    for (int t = 0; t < 2 * QUARTER; ++t) load_a(t);
+#pragma unroll
+    for (int t = 0; t < QUARTER; ++t) load_b(t);
+    __builtin_amdgcn_s_waitcnt(0);
+    barrier();
+    Frags F0, F1;
+    int c_sa = 0, c_sb = 1;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) read_one(c_sa, c_sb, 0, q, F0);
+    while (true) {
+        f32x16 acc[4][4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-        bf16x8 fw[BK / 16][4], fa[BK / 16][2];
-        auto read_frags = [&](int kt) {
-            const char* stage = smem + (kt & 1) * STAGE_B;
+            for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+        // One sub-step: the 16 MFMAs on `cur`, with the 8 fragment reads of the next sub-step
+        // (into `nxt`) after every other MFMA and one load after every fourth, in a fixed
+        // order: the reads and loads issue while the matrix core works.
+        auto substep = [&](const Frags& cur, Frags& nxt, int rsa, int rsb, int rks, int ld_kind, int ld_t0) {
 #pragma unroll
-            for (int ks = 0; ks < BK / 16; ++ks) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    fw[ks][i] = *reinterpret_cast<const bf16x8*>(stage + b_lds[ks ^ (2 * (i & 1))] + i * 32 * ROW_B);
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    fa[ks][j] = *reinterpret_cast<const bf16x8*>(stage + a_lds[ks ^ (2 * (j & 1))] + j * 32 * ROW_B);
-            }
-        };
-        auto mfmas = [&]() {
-            __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-            for (int ks = 0; ks < BK / 16; ++ks)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < 2; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[ks][i], fa[ks][j], acc[i][j], 0, 0, 0);
-            __builtin_amdgcn_s_setprio(0);
-        };
-
-        // ---- ping-pong over K.  Group 0 runs [memory, MFMA] phases; group 1 runs the same
-        // one phase later, so on every SIMD one wavefront issues MFMAs while the other reads
-        // LDS.  Tile kt+1 is requested in phase 2kt (group 0 in its memory phase, group 1 at
-        // the end of its MFMA phase) and waited for at the end of phase 2kt+1; a stage is
-        // refilled only after both groups have read it.  Both groups execute 2 nk + 2
-        // barriers, and every LDS read of the tile has completed before the last one, so the
-        // next tile may refill either stage right after it.
-        // Waits never rely on loads retiring in issue order across descriptors: group 0's A
-        // loads (rows past M read as zero) are waited for with vmcnt(0); group 1's B loads
-        // are all in range, and it keeps only the next stage's LOADS loads in flight.
-        issue_loads(0);
-        __builtin_amdgcn_s_waitcnt(0);
-        barrier();
-        if (grp == 0) {
-            for (int kt = 0; kt < nk; ++kt) {
-                read_frags(kt);
-                if (kt + 1 < nk) issue_loads(kt + 1);        // after the LDS reads: they start first
-                __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
-                barrier();
-                mfmas();
-                __builtin_amdgcn_s_waitcnt(0x0f70);          // vmcnt(0): this group's part of tile kt+1
-                barrier();
-            }
-            barrier();
-        } else {
-            if (nk > 1) issue_loads(1);
-            barrier();
-            for (int kt = 0; kt < nk; ++kt) {
-                read_frags(kt);
-                // Tile kt+2 goes to the stage this group has just finished reading (group 0 read
-                // it in phase 2kt), so its loads are issued here, in this group's memory phase:
-                // group 0 issues its loads in the other phase, and the CU's single address unit
-                // then sees half of a K step's loads in each phase.  They are waited for one
-                // iteration later, so they have two phases to land.
-                __builtin_amdgcn_s_waitcnt(0xc07f);          // lgkmcnt(0): fragments in registers
-                if (kt + 2 < nk) {
-                    issue_loads(kt + 2);
-                    __builtin_amdgcn_s_waitcnt(0x0f78);      // vmcnt(8): tile kt+1 landed, kt+2 in flight
-                } else {
-                    __builtin_amdgcn_s_waitcnt(0x0f70);      // vmcnt(0)
+            for (int m = 0; m < 16; ++m) {
+                const int i = m >> 2, j = m & 3;
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.w[i], cur.a[j], acc[i][j], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                if ((m & 1) == 0) read_one(rsa, rsb, rks, m >> 1, nxt);
+                if ((m & 3) == 1) {
+                    if (ld_kind == 0) load_a(ld_t0 + (m >> 2));
+                    else load_b(ld_t0 + (m >> 2));
                 }
-                barrier();
-                mfmas();
-                barrier();
+                __builtin_amdgcn_sched_barrier(0);
             }
+        };
+        for (int kt = 0; kt < nk; ++kt) {
+            const int n_sa = c_sa >= NSLOT - 2 ? c_sa + 2 - NSLOT : c_sa + 2;
+            const int n_sb = c_sb >= NSLOT - 2 ? c_sb + 2 - NSLOT : c_sb + 2;
+            substep(F0, F1, c_sa, c_sb, 1, 1, QUARTER);   // B of g+1, loads 4-7
+            advance_cursor();                             // the cursor moves to step g+2
+            substep(F1, F0, c_sa, c_sb, 2, 0, 0);         // A of g+2, loads 0-3
+            substep(F0, F1, c_sa, c_sb, 3, 0, QUARTER);   // A of g+2, loads 4-7
+            if (l_local < n_local) __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(8));
+            else __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+            barrier();
+            substep(F1, F0, n_sa, n_sb, 0, 1, 0);         // B of g+2, loads 0-3
+            c_sa = n_sa;
+            c_sb = n_sb;
         }
-        epilogue<EPI>(acc, Cv, ldc, M, m0, n0, wm, wn, fr, fh, slot_seg, qo);
+        // The slot of the last step's B tile is free until the A tile of step g+3 (its next
+        // user) is requested in the next step's second sub-step; wavefront w's staging area
+        // is exactly the part of it that w's own loads refill.
+        const int m0 = tile_m0(c_local), n0 = tile_n0(c_local);
+        const int free_slot = c_sb >= 2 ? c_sb - 2 : c_sb + NSLOT - 2;
+        epilogue<EPI>(acc, Cv, ldc, M, m0 + wm * 128, n0 + wn * 128, lane, slot_seg, qo,
+                      smem + free_slot * SLOT_B + wave * 2 * QUARTER * 1024);
+        c_local = next_active(c_local + n_slots);
+        if (c_local >= n_local) break;
     }
     __builtin_amdgcn_s_waitcnt(0);   // no load may still be writing LDS when the workgroup ends
 }
@@ -351,7 +441,7 @@ void launch(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int
     }();
     (void)attr;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
-    // one workgroup per CU (each needs 128 KB of LDS, so a CU holds one), a multiple of 8 so
+    // one workgroup per CU (each needs the whole 160 KB LDS), a multiple of 8 so
     // that every XCD runs the same number; never more workgroups than tiles
     static const int n_cu = [] {
         int dev = 0, n = 0;
