@@ -5,27 +5,29 @@
 // weight matrix in [out, in] layout (bf16, K contiguous), float32 accumulation.
 //
 // Tiling: one 256-thread workgroup (4 wavefronts, one per SIMD) per 256 x 256 output tile,
-// K consumed in steps of 64.  Each wavefront owns a 128 (N) x 128 (M) sub-tile = 4 x 4
-// blocks of the 32x32x16 bf16 MFMA; its 256 float32 accumulators live in the accumulation
-// registers.  The weight block is the MFMA's first operand, so a lane's accumulators are
-// 4-element runs along N of one activation row: the epilogue writes 8-byte (bf16) or
-// 16-byte (float32) runs without a transpose.
+// K consumed in steps of 64.  Each wavefront owns a 128 (N) x 128 (M) sub-tile = 8 x 8
+// blocks of the 16x16x32 bf16 MFMA; its 256 float32 accumulators live in the accumulation
+// registers.  (Under the chip's power limit the 16x16x32 form sustains a higher clock than
+// 32x32x16 for the same work: it moves half the accumulator bytes per flop.)  The weight
+// block is the MFMA's first operand, so a lane's accumulators are 4-element runs along N of
+// one activation row.
 //
 // Data path: operand tiles go straight from global memory into LDS (buffer loads with the
 // LDS destination, no staging registers), whole 128-byte row segments per request.  The LDS
 // is a ring of 5 slots of 32 KB, each holding one operand (A or B) of one K-step; slots are
-// filled in the order A0 B0 A1 B1 ... and freed in pairs when a step has been read, so the
-// A tile of step g+2 is already loading while step g is consumed.  The workgroup's tiles
-// form one continuous stream of K-steps: the loads cross tile boundaries, and the first
-// steps of the next tile land while the epilogue of the current one runs.  A step is four
-// sub-steps of 16 MFMAs per wavefront; each sub-step also reads the MFMA fragments of the
-// next sub-step from LDS and issues a quarter of an operand tile (4 loads per wavefront),
-// which keeps the CU's address unit about half busy at all times.  One barrier per step.
+// filled in the order A0 B0 A1 B1 ... and freed in pairs when a step has been read, so two
+// operand tiles are always in flight while a step is consumed.  The workgroup's tiles form
+// one continuous stream of K-steps: the loads cross tile boundaries, and the first steps of
+// the next tile land while the epilogue of the current one runs.  A step is two sub-steps of
+// 64 MFMAs per wavefront; each sub-step also reads the fragments of the next sub-step from
+// LDS and issues one operand tile (8 loads per wavefront), which keeps the CU's address
+// unit about half busy at all times.  One barrier per step.
 //
 // Epilogues: bf16 store; float32 residual add; SwiGLU over interleaved gate/up blocks; and,
 // for the QKV projection, RoPE at the restart positions (section 3.2) applied to the float32
 // accumulators, with queries stored to the packed batch and keys and values stored straight
-// into the per-prompt caches (the UNPACK of Algorithm 1).
+// into the per-prompt caches (the UNPACK of Algorithm 1).  bf16 results are staged through
+// LDS and stored as whole rows.
 //
 // Scheduling: persistent, one workgroup per CU.  Workgroups are dealt to the 8 XCDs
 // round-robin, so XCD x runs workgroups x, x + 8, ...; each XCD owns a contiguous block of
@@ -45,8 +47,8 @@ constexpr int ROW_B = BK * 2;            // LDS row: 128 bytes = 8 chunks of 16 
 constexpr int SLOT_B = BM * ROW_B;       // one operand of one K-step (32 KB)
 constexpr int NSLOT = 5;                 // the whole 160 KB LDS of a CU
 constexpr int LDS_BYTES = NSLOT * SLOT_B;
-constexpr int QUARTER = SLOT_B / 1024 / 4 / 2;   // 1 KB loads per wavefront per quarter operand (4)
-static_assert(QUARTER == 4, "the vmcnt wait of the K loop counts 8 loads per operand tile");
+constexpr int LOADS = SLOT_B / 1024 / 4; // 1 KB loads per wavefront per operand tile (8)
+static_assert(LOADS == 8, "the vmcnt wait of the K loop counts 8 loads per operand tile");
 
 // s_waitcnt immediate: vmcnt(n) and lgkmcnt(0), expcnt not waited for (gfx9 encoding:
 // vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
@@ -54,10 +56,16 @@ constexpr int wait_vm_lgkm0(int n) { return ((n >> 4) << 14) | (n & 15) | 0x0070
 // Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
 constexpr int kRsrcWord3 = 0x00020000;
 
-// LDS swizzle: logical 16-byte chunk c of tile row r is stored at chunk c ^ f(r).  With
-// f(r) = (r ^ r>>3) & 7, the 32 rows x one chunk read by a half-wavefront for an MFMA
-// fragment hit distinct banks whether the LDS serves 8 or 16 lanes per cycle.
-__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+// LDS swizzle: logical 16-byte chunk c of tile row r is stored at chunk c ^ f(r), where f's
+// bits are r's bits 1, 3 and 2.  An MFMA fragment read (ds_read_b128) fetches chunks
+// 4 ks + l / 16 of rows l % 16; the LDS serves it 16 lanes (256 bytes, all 64 banks) per
+// cycle, taking lanes i and i + 32 together (lanes 0-7 with 32-39, and so on), which is
+// 8 rows x chunks {c, c ^ 2}.  A 128-byte row covers half the banks, so the 16 accesses are
+// conflict-free when (r % 2, physical chunk) are distinct: within each parity the four rows
+// must give f values in distinct classes {x, x ^ 2}, i.e. distinct (bit 0, bit 2) of f,
+// which are r's bits 1 and 2.  (The same f is also conflict-free if the LDS took 16
+// consecutive lanes.)  f depends on r % 16 only.
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 1) | (((r >> 3) & 1) << 1) | (r & 4); }
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -74,52 +82,56 @@ __device__ __forceinline__ void barrier() {
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// The accumulators of activation block j, pinned in the accumulation registers at this point:
-// the epilogue then moves them to vector registers one block at a time instead of all at once
-// (which would need every vector register and spill).  The accumulators are dead afterwards.
-__device__ __forceinline__ void take_block(f32x16 (&acc)[4][4], int j, f32x16 (&c)[4]) {
+// The accumulators of activation blocks 2 jp and 2 jp + 1, pinned in the accumulation
+// registers at this point: the epilogue then moves them to vector registers a pair of blocks
+// at a time instead of all at once (which would need every vector register and spill).  The
+// accumulators are dead afterwards.
+__device__ __forceinline__ void take_pair(f32x4 (&acc)[8][8], int jp, f32x4 (&c)[8][2]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        asm volatile("" : "+a"(acc[i][j]) : : "memory");
-        c[i] = acc[i][j];
-    }
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            asm volatile("" : "+a"(acc[i][2 * jp + h]) : : "memory");
+            c[i][h] = acc[i][2 * jp + h];
+        }
 }
 
-// Staged bf16 output of one activation block: 32 rows x `cols` bf16 written by the lanes in
-// MFMA layout to this wavefront's LDS staging area, then read back as whole 16-byte chunks of
-// rows and stored with each instruction covering complete rows (full cache lines).  Row r's
-// 16-byte chunk c sits at chunk c ^ (r % chunks) of the staging row.
+// Staged bf16 output of 32 activation rows: lanes write 8-byte runs in MFMA layout to this
+// wavefront's LDS staging area, then read back whole 16-byte chunks of rows and store them
+// with each instruction covering complete rows (full cache lines).  Row r's 16-byte chunk c
+// sits at chunk c ^ (r % CHUNKS) of the staging row.
 template <int CHUNKS>
-__device__ __forceinline__ void stage_put(char* stg, int r, int c, int fh, bf16x4 v) {
-    *reinterpret_cast<bf16x4*>(stg + r * CHUNKS * 16 + ((c ^ (r % CHUNKS)) * 16) + fh * 8) = v;
+__device__ __forceinline__ void stage_put(char* stg, int r, int c, int half, bf16x4 v) {
+    *reinterpret_cast<bf16x4*>(stg + r * CHUNKS * 16 + ((c ^ (r % CHUNKS)) * 16) + half * 8) = v;
 }
 
-// The epilogue of one wavefront sub-tile (activation rows mb.., weight rows nb0..): the lane
-// holds, for activation rows m (four, one per j), runs of 4 consecutive n of four 32-column
-// blocks.  stg is this wavefront's 8 KB of LDS, free for the duration of the epilogue.
+// The epilogue of one wavefront sub-tile (activation rows mb.., weight rows nb0..).  In block
+// (i, j) lane l holds activation row mb + 16 j + l % 16 and the 4 consecutive weight rows
+// nb0 + 16 i + 4 (l / 16) + 0..3.  stg is this wavefront's 8 KB of LDS, free for the duration
+// of the epilogue.
 template <int EPI>
-__device__ __forceinline__ void epilogue(f32x16 (&acc)[4][4], void* __restrict__ Cv, int64_t ldc, int M,
+__device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ Cv, int64_t ldc, int M,
                                          int mb, int nb0, int lane, const int32_t* __restrict__ slot_seg,
                                          const ppk::QkvOut& qo, char* stg) {
-    const int fr = lane & 31, fh = lane >> 5;
+    const int lr = lane & 15, g = lane >> 4;
     if constexpr (EPI == ppk::kResidual) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            f32x16 cj[4];
-            take_block(acc, j, cj);
-            const int m = mb + j * 32 + fr;
-            if (m >= M) continue;
-            float* C = static_cast<float*>(Cv) + int64_t(m) * ldc + nb0;
+        for (int jp = 0; jp < 4; ++jp) {
+            f32x4 c[8][2];
+            take_pair(acc, jp, c);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int h = 0; h < 2; ++h) {
+                const int m = mb + 32 * jp + 16 * h + lr;
+                if (m >= M) continue;
+                float* C = static_cast<float*>(Cv) + int64_t(m) * ldc + nb0 + 4 * g;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    f32x4* p = reinterpret_cast<f32x4*>(C + i * 32 + q * 8 + fh * 4);
+                for (int i = 0; i < 8; ++i) {
+                    f32x4* p = reinterpret_cast<f32x4*>(C + 16 * i);
                     f32x4 v = *p;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] += cj[i][q * 4 + e];
+                    v += c[i][h];
                     *p = v;
                 }
+            }
         }
         return;
     }
@@ -128,66 +140,65 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[4][4], void* __restrict__
     int head = 0, kind = 0;
     if constexpr (EPI == ppk::kQkvRope) {
         // The wavefront's 128 columns are exactly one head (tiles start at multiples of 256),
-        // and the rotate-half partners c and c + 64 are accumulator blocks i and i + 2 of the
+        // and the rotate-half partners c and c + 64 are accumulator blocks i and i + 4 of the
         // same lane: RoPE is applied to the float32 accumulators before the one rounding.
         head = nb0 >> 7;
         kind = head < qo.H ? 0 : (head < qo.H + qo.Hkv ? 1 : 2);   // q, k, v (uniform)
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        f32x16 c[4];
-        take_block(acc, j, c);
-        const int m = mb + j * 32 + fr;
-        int dst_row = m;   // row of the destination that activation row m goes to (< 0: none)
-        if constexpr (EPI == ppk::kQkvRope) {
-            if (kind > 0) dst_row = m < M ? qo.slot_kv[m] : -1;
-            if (kind < 2) {
-                const int pos = m < M && slot_seg[m] >= 0 ? qo.slot_pos[m] : 0;
-                const float2* cs = qo.table + int64_t(pos) * 64 + fh * 4;
+    for (int jp = 0; jp < 4; ++jp) {
+        f32x4 c[8][2];
+        take_pair(acc, jp, c);
+        int dst_row[2];   // destination rows of this lane's two activation rows (< 0: none)
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
+        for (int h = 0; h < 2; ++h) {
+            const int m = mb + 32 * jp + 16 * h + lr;
+            const int r = 16 * h + lr;   // row in the staging block
+            dst_row[h] = m;
+            if constexpr (EPI == ppk::kQkvRope) {
+                if (kind > 0) dst_row[h] = m < M ? qo.slot_kv[m] : -1;
+                if (kind < 2) {
+                    const int pos = m < M && slot_seg[m] >= 0 ? qo.slot_pos[m] : 0;
+                    const float2* cs = qo.table + int64_t(pos) * 64 + 4 * g;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const f32x4 t0 = *reinterpret_cast<const f32x4*>(cs + i * 32 + q * 8);
-                        const f32x4 t1 = *reinterpret_cast<const f32x4*>(cs + i * 32 + q * 8 + 2);
+                    for (int i = 0; i < 4; ++i) {
+                        const f32x4 t0 = *reinterpret_cast<const f32x4*>(cs + 16 * i);
+                        const f32x4 t1 = *reinterpret_cast<const f32x4*>(cs + 16 * i + 2);
                         const float cv[4] = {t0[0], t0[2], t1[0], t1[2]};
                         const float sv[4] = {t0[1], t0[3], t1[1], t1[3]};
                         bf16x4 lo, hi;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            const float a = c[i][q * 4 + e], b = c[i + 2][q * 4 + e];
+                            const float a = c[i][h][e], b = c[i + 4][h][e];
                             lo[e] = static_cast<bf16>(a * cv[e] - b * sv[e]);
                             hi[e] = static_cast<bf16>(b * cv[e] + a * sv[e]);
                         }
-                        stage_put<CH>(stg, fr, i * 4 + q, fh, lo);
-                        stage_put<CH>(stg, fr, 8 + i * 4 + q, fh, hi);
+                        stage_put<CH>(stg, r, 2 * i + (g >> 1), g & 1, lo);
+                        stage_put<CH>(stg, r, 8 + 2 * i + (g >> 1), g & 1, hi);
                     }
+                }
+            }
+            if constexpr (EPI == ppk::kSwiGLU) {
+                // weight rows 32 k .. +15 (block 2 k) are gate rows, 32 k + 16 .. +31 (block
+                // 2 k + 1) the matching up rows: output column 16 k + 4 g + e
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    bf16x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(silu_rcp(c[2 * k][h][e]) * c[2 * k + 1][h][e]);
+                    stage_put<CH>(stg, r, 2 * k + (g >> 1), g & 1, v);
+                }
+            } else if (EPI == ppk::kStore || kind == 2) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    bf16x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(c[i][h][e]);
+                    stage_put<CH>(stg, r, 2 * i + (g >> 1), g & 1, v);
+                }
             }
         }
-        if constexpr (EPI == ppk::kSwiGLU) {
-            // rows 32 i .. +15 of block i are gate rows, 32 i + 16 .. +31 the matching up rows:
-            // output column 16 i + 8 q + 4 fh + e
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int q = 0; q < 2; ++q) {
-                    bf16x4 v;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(silu_rcp(c[i][q * 4 + e]) * c[i][(q + 2) * 4 + e]);
-                    stage_put<CH>(stg, fr, i * 2 + q, fh, v);
-                }
-        } else if (EPI == ppk::kStore || kind == 2) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    bf16x4 v;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(c[i][q * 4 + e]);
-                    stage_put<CH>(stg, fr, i * 4 + q, fh, v);
-                }
-        }
-        // read back whole rows: instruction k covers rows (64 / CH) k .. of the block
+        // read back whole rows: instruction k covers rows (64 / CH) k .. of the 32-row block
         constexpr int RPI = 64 / CH;   // rows per instruction
         bf16x8 v[32 / RPI];
 #pragma unroll
@@ -198,9 +209,11 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[4][4], void* __restrict__
 #pragma unroll
         for (int k = 0; k < 32 / RPI; ++k) {
             const int r = k * RPI + lane / CH, ch = lane % CH;
-            const int mr = mb + j * 32 + r;
+            const int mr = mb + 32 * jp + r;
             if constexpr (EPI == ppk::kQkvRope) {
-                const int drow = __shfl(dst_row, r);   // lane r holds row r's destination
+                // lane r % 16 holds row r's destination (in dst_row[r / 16])
+                const int d0 = __shfl(dst_row[0], r & 15), d1 = __shfl(dst_row[1], r & 15);
+                const int drow = r < 16 ? d0 : d1;
                 if (mr >= M || drow < 0) continue;
                 bf16* dst = kind == 0 ? static_cast<bf16*>(qo.q) + int64_t(drow) * qo.ldq + head * 128
                                       : static_cast<bf16*>(kind == 1 ? qo.kc : qo.vc) + int64_t(drow) * qo.ldkv +
@@ -262,21 +275,20 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
 
     // ---- direct global -> LDS loads.  Load t (0..7) of wavefront w fills 1 KB = rows
     // 64 w + 8 t .. + 7 of an operand tile; lane l lands at physical chunk l % 8 of row
-    // 64 w + 8 t + l / 8 and fetches the logical chunk that the swizzle puts there
-    // (f = (l / 8) ^ t for these rows).  Rows of A past M are read as row M - 1: every load is
-    // in range, so loads complete in the order they were issued, and the results of the
-    // duplicated rows are never stored.
+    // 64 w + 8 t + l / 8 and fetches the logical chunk that the swizzle puts there.  Rows of
+    // A past M are read as row M - 1: every load is in range, so loads complete in the order
+    // they were issued, and the results of the duplicated rows are never stored.
     const int64_t lda2 = lda * 2, ldb2 = ldb * 2;
     const int lrow = lane >> 3;
-    int chunk_off[2 * QUARTER], voff_b[2 * QUARTER], voff_a[2 * QUARTER];
+    int chunk_off[LOADS], voff_b[LOADS], voff_a[LOADS];
 #pragma unroll
-    for (int t = 0; t < 2 * QUARTER; ++t) {
-        chunk_off[t] = 16 * ((lane & 7) ^ lrow ^ t);
+    for (int t = 0; t < LOADS; ++t) {
+        chunk_off[t] = 16 * ((lane & 7) ^ swz(8 * (t & 1) + lrow));
         voff_b[t] = static_cast<int>((64 * wave + 8 * t + lrow) * ldb2) + chunk_off[t];
     }
 
-    // load cursor: the K-step whose operand tiles are being requested, in slots l_sa (A) and
-    // l_sb (B); l_local >= n_local once the stream is exhausted (its loads are then dead:
+    // load cursor: the K-step whose operand tiles are being requested, into slots l_sa (A)
+    // and l_sb (B); l_local >= n_local once the stream is exhausted (its loads are then dead:
     // they read nothing and land in slots that are never read again)
     int l_local = next_active(slot), l_kt = 0, l_sa = 0, l_sb = 1;
     __amdgpu_buffer_rsrc_t rsrc_a, rsrc_b;
@@ -290,7 +302,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
             rsrc_b = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(B + int64_t(n0) * ldb), 0,
                                                        static_cast<int>(BN * ldb2), kRsrcWord3);
 #pragma unroll
-            for (int t = 0; t < 2 * QUARTER; ++t)
+            for (int t = 0; t < LOADS; ++t)
                 voff_a[t] = static_cast<int>(min(64 * wave + 8 * t + lrow, a_rows - 1) * lda2) + chunk_off[t];
         } else {
             rsrc_a = rsrc_0;
@@ -299,11 +311,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
     };
     set_cursor_tile();
     auto load_a = [&](int t) {
-        char* dst = smem + l_sa * SLOT_B + (wave * 2 * QUARTER + t) * 1024;
+        char* dst = smem + l_sa * SLOT_B + (wave * LOADS + t) * 1024;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_a, (lds_void*)dst, 16, voff_a[t], l_kt * BK * 2, 0, 0);
     };
     auto load_b = [&](int t) {
-        char* dst = smem + l_sb * SLOT_B + (wave * 2 * QUARTER + t) * 1024;
+        char* dst = smem + l_sb * SLOT_B + (wave * LOADS + t) * 1024;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_b, (lds_void*)dst, 16, voff_b[t], l_kt * BK * 2, 0, 0);
     };
     auto advance_cursor = [&]() {
@@ -317,81 +329,77 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
         }
     };
 
-    // ---- wavefront sub-tile: 128 (N) x 128 (M) = 4 x 4 MFMA blocks of 32 x 32
+    // ---- wavefront sub-tile: 128 (N) x 128 (M) = 8 x 8 MFMA blocks of 16 x 16.  A fragment
+    // of block i for sub-step ks: row base + 16 i + l % 16 (base a multiple of 128), logical
+    // chunk 4 ks + l / 16 of the step's 128-byte row.  The row's swizzle depends on l % 16
+    // only, so one per-lane offset per sub-step covers all blocks; the block stride (16 rows
+    // = 2 KB) is immediate.
     const int wn = wave & 1, wm = wave >> 1;
-    const int fr = lane & 31, fh = lane >> 5;
-    // fragment addresses.  Row r = base + 32 i + fr of either operand has swizzle
-    // f(r) = g ^ 4 (i & 1) with g = ((fr & 7) ^ (fr >> 3)) & 7 (base is a multiple of 128), so
-    // the physical chunk of logical chunk 2 ks + fh is (2 (ks ^ 2 (i & 1))) ^ (fh ^ g): four
-    // per-lane offsets cover every (ks, i); the block stride (32 rows = 4 KB) is immediate.
-    const int x = fh ^ (((fr & 7) ^ (fr >> 3)) & 7);
-    int a_lds[4], b_lds[4];
+    int a_lds[2], b_lds[2];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        a_lds[m] = (wm * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
-        b_lds[m] = (wn * 128 + fr) * ROW_B + 16 * ((2 * m) ^ x);
+    for (int ks = 0; ks < 2; ++ks) {
+        const int phys = ((4 * ks + (lane >> 4)) ^ swz(lane & 15)) * 16;
+        a_lds[ks] = (wm * 128 + (lane & 15)) * ROW_B + phys;
+        b_lds[ks] = (wn * 128 + (lane & 15)) * ROW_B + phys;
     }
-    struct Frags { bf16x8 w[4], a[4]; };
+    struct Frags { bf16x8 w[8], a[8]; };
     // fragment q of sub-step ks of the step held in slots (sa, sb), in the order the MFMAs
-    // first need them: w0, a0..a3, w1..w3
+    // first need them: w0, a0..a7, w1..w7
     auto read_one = [&](int sa, int sb, int ks, int q, Frags& f) {
         if (q == 0) {
             f.w[0] = *reinterpret_cast<const bf16x8*>(smem + sb * SLOT_B + b_lds[ks]);
-        } else if (q < 5) {
+        } else if (q < 9) {
             const int j = q - 1;
-            f.a[j] = *reinterpret_cast<const bf16x8*>(smem + sa * SLOT_B + a_lds[ks ^ (2 * (j & 1))] + j * 32 * ROW_B);
+            f.a[j] = *reinterpret_cast<const bf16x8*>(smem + sa * SLOT_B + a_lds[ks] + j * 16 * ROW_B);
         } else {
-            const int i = q - 4;
-            f.w[i] = *reinterpret_cast<const bf16x8*>(smem + sb * SLOT_B + b_lds[ks ^ (2 * (i & 1))] + i * 32 * ROW_B);
+            const int i = q - 8;
+            f.w[i] = *reinterpret_cast<const bf16x8*>(smem + sb * SLOT_B + b_lds[ks] + i * 16 * ROW_B);
         }
     };
 
     // ---- the K-step stream.  Step g holds slots 2g % 5 (A) and (2g+1) % 5 (B).  Per step:
-    //   sub-step 0: MFMAs (g, 0); read (g, 1); B tile of step g+1, loads 4-7
-    //   sub-step 1: MFMAs (g, 1); read (g, 2); A tile of step g+2, loads 0-3
-    //   sub-step 2: MFMAs (g, 2); read (g, 3); A tile of step g+2, loads 4-7
+    //   sub-step 0: MFMAs (g, 0); read (g, 1); A tile of step g+2 (into the slot of B of g-1)
     //   wait until step g+1 has landed and this wavefront's reads of step g are done; barrier
-    //   sub-step 3: MFMAs (g, 3); read (g+1, 0); B tile of step g+2, loads 0-3
-    // The slots of step g are free after the barrier; the B tile of g+2 is the first load to
-    // reuse one of them.  At the barrier the only loads issued after step g+1's are the 8 of
-    // the A tile of g+2, so vmcnt(8) (vmcnt(0) when g+2 does not exist) waits for g+1 exactly.
+    //   sub-step 1: MFMAs (g, 1); read (g+1, 0); B tile of step g+2 (into the slot of A of g)
+    // The B tile of g+1 was requested right after the previous barrier, one sub-step before
+    // the A tile of g+2; at this barrier the loads issued after it are the 8 of the A tile of
+    // g+2, so vmcnt(8) (vmcnt(0) when g+2 does not exist) waits for g+1 exactly.
     int c_local = l_local;
     if (c_local >= n_local) return;
-    // prologue: steps 0 (A, B) and 1 (A, B loads 0-3)
+    // prologue: steps 0 and 1
 #pragma unroll
-    for (int t = 0; t < 2 * QUARTER; ++t) load_a(t);
+    for (int p = 0; p < 2; ++p) {
 #pragma unroll
-    for (int t = 0; t < 2 * QUARTER; ++t) load_b(t);
-    advance_cursor();
+        for (int t = 0; t < LOADS; ++t) load_a(t);
 #pragma unroll
-    for (int t = 0; t < 2 * QUARTER; ++t) load_a(t);
-#pragma unroll
-    for (int t = 0; t < QUARTER; ++t) load_b(t);
+        for (int t = 0; t < LOADS; ++t) load_b(t);
+        advance_cursor();
+    }
     __builtin_amdgcn_s_waitcnt(0);
     barrier();
     Frags F0, F1;
     int c_sa = 0, c_sb = 1;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) read_one(c_sa, c_sb, 0, q, F0);
+    for (int q = 0; q < 16; ++q) read_one(c_sa, c_sb, 0, q, F0);
     while (true) {
-        f32x16 acc[4][4];
+        f32x4 acc[8][8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
-        // One sub-step: the 16 MFMAs on `cur`, with the 8 fragment reads of the next sub-step
-        // (into `nxt`) after every other MFMA and one load after every fourth, in a fixed
+            for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{};
+        // One sub-step: the 64 MFMAs on `cur`, with the 16 fragment reads of the next sub-step
+        // (into `nxt`) after every fourth MFMA and one load after every eighth, in a fixed
         // order: the reads and loads issue while the matrix core works.
-        auto substep = [&](const Frags& cur, Frags& nxt, int rsa, int rsb, int rks, int ld_kind, int ld_t0) {
+        auto substep = [&](const Frags& cur, Frags& nxt, int rsa, int rsb, int rks, bool ld_a) {
 #pragma unroll
-            for (int m = 0; m < 16; ++m) {
-                const int i = m >> 2, j = m & 3;
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.w[i], cur.a[j], acc[i][j], 0, 0, 0);
+            for (int m = 0; m < 64; ++m) {
+                const int i = m >> 3, j = m & 7;
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.w[i], cur.a[j], acc[i][j], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
-                if ((m & 1) == 0) read_one(rsa, rsb, rks, m >> 1, nxt);
-                if ((m & 3) == 1) {
-                    if (ld_kind == 0) load_a(ld_t0 + (m >> 2));
-                    else load_b(ld_t0 + (m >> 2));
+                if ((m & 3) == 0) read_one(rsa, rsb, rks, m >> 2, nxt);
+                if ((m & 7) == 2) {
+                    if (ld_a) load_a(m >> 3);
+                    else load_b(m >> 3);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -399,24 +407,22 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
         for (int kt = 0; kt < nk; ++kt) {
             const int n_sa = c_sa >= NSLOT - 2 ? c_sa + 2 - NSLOT : c_sa + 2;
             const int n_sb = c_sb >= NSLOT - 2 ? c_sb + 2 - NSLOT : c_sb + 2;
-            substep(F0, F1, c_sa, c_sb, 1, 1, QUARTER);   // B of g+1, loads 4-7
-            advance_cursor();                             // the cursor moves to step g+2
-            substep(F1, F0, c_sa, c_sb, 2, 0, 0);         // A of g+2, loads 0-3
-            substep(F0, F1, c_sa, c_sb, 3, 0, QUARTER);   // A of g+2, loads 4-7
-            if (l_local < n_local) __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(8));
+            substep(F0, F1, c_sa, c_sb, 1, true);    // A tile of g+2
+            if (l_local < n_local) __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(LOADS));
             else __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
             barrier();
-            substep(F1, F0, n_sa, n_sb, 0, 1, 0);         // B of g+2, loads 0-3
+            substep(F1, F0, n_sa, n_sb, 0, false);   // B tile of g+2
+            advance_cursor();                        // the cursor moves to step g+3
             c_sa = n_sa;
             c_sb = n_sb;
         }
         // The slot of the last step's B tile is free until the A tile of step g+3 (its next
-        // user) is requested in the next step's second sub-step; wavefront w's staging area
-        // is exactly the part of it that w's own loads refill.
+        // user) is requested in the next step's first sub-step; wavefront w's staging area is
+        // exactly the part of it that w's own loads refill.
         const int m0 = tile_m0(c_local), n0 = tile_n0(c_local);
         const int free_slot = c_sb >= 2 ? c_sb - 2 : c_sb + NSLOT - 2;
         epilogue<EPI>(acc, Cv, ldc, M, m0 + wm * 128, n0 + wn * 128, lane, slot_seg, qo,
-                      smem + free_slot * SLOT_B + wave * 2 * QUARTER * 1024);
+                      smem + free_slot * SLOT_B + wave * LOADS * 1024);
         c_local = next_active(c_local + n_slots);
         if (c_local >= n_local) break;
     }
