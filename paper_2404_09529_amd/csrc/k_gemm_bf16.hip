@@ -388,17 +388,23 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
 #pragma unroll
             for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{};
         // One sub-step: the 64 MFMAs on `cur`, with the 16 fragment reads of the next sub-step
-        // (into `nxt`) after every fourth MFMA and one load after every eighth, in a fixed
-        // order: the reads and loads issue while the matrix core works.
-        auto substep = [&](const Frags& cur, Frags& nxt, int rsa, int rsb, int rks, bool ld_a) {
+        // (into `nxt`) and one load after every eighth MFMA, in a fixed order: the reads and
+        // loads issue while the matrix core works.  The first sub-step (A loads) ends at the
+        // barrier: its reads go after every third of the first 48 MFMAs, so they have landed
+        // by the time the barrier's wait checks them; the second spreads them over all 64.
+        auto substep = [&](const Frags& cur, Frags& nxt, int rsa, int rsb, int rks, bool first) {
 #pragma unroll
             for (int m = 0; m < 64; ++m) {
                 const int i = m >> 3, j = m & 7;
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.w[i], cur.a[j], acc[i][j], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
-                if ((m & 3) == 0) read_one(rsa, rsb, rks, m >> 2, nxt);
+                if (first) {
+                    if (m % 3 == 0 && m < 48) read_one(rsa, rsb, rks, m / 3, nxt);
+                } else {
+                    if ((m & 3) == 0) read_one(rsa, rsb, rks, m >> 2, nxt);
+                }
                 if ((m & 7) == 2) {
-                    if (ld_a) load_a(m >> 3);
+                    if (first) load_a(m >> 3);
                     else load_b(m >> 3);
                 }
                 __builtin_amdgcn_sched_barrier(0);
