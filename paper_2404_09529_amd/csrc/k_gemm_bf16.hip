@@ -115,24 +115,55 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
                                          const ppk::QkvOut& qo, char* stg) {
     const int lr = lane & 15, g = lane >> 4;
     if constexpr (EPI == ppk::kResidual) {
+        // C[m][nb0 ..] += this lane's accumulators, one 16-row block j at a time, staged
+        // through LDS (16 rows x 128 floats, 512-byte rows) so that C is read and written as
+        // whole rows: instruction k covers rows 2 k and 2 k + 1, 16 bytes per lane.  The C
+        // rows of block j + 1 are requested before block j is stored: vmcnt counts stores and
+        // completes in order, so a load issued after a store would wait for the store.
+        // Staging row r's 16-byte chunk q sits at q ^ f(r), f = (r0 << 3) | (r1 << 2) | r2
+        // (r's low bits): the MFMA-layout writes (rows r, chunks 4 i + g and 4 i + g ^ 2 per
+        // pair of lane groups) and the row reads (rows 2 k and 2 k + 1, chunks 0..7 or 8..15
+        // per pair) both land on distinct banks.
+        auto f = [](int r) { return ((r & 1) << 3) | (((r >> 1) & 1) << 2) | ((r >> 2) & 1); };
+        float* C = static_cast<float*>(Cv);
+        const int half = lane >> 5, col = nb0 + 4 * (lane & 31);
+        f32x4 cbuf[2][8];
+        auto load_block = [&](int j, f32x4 (&buf)[8]) {
 #pragma unroll
-        for (int jp = 0; jp < 4; ++jp) {
-            f32x4 c[8][2];
-            take_pair(acc, jp, c);
+            for (int k = 0; k < 8; ++k) {
+                const int m = min(mb + 16 * j + 2 * k + half, M - 1);   // rows past M: read, not stored
+                buf[k] = *reinterpret_cast<const f32x4*>(C + int64_t(m) * ldc + col);
+            }
+        };
+        load_block(0, cbuf[0]);
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int m = mb + 32 * jp + 16 * h + lr;
-                if (m >= M) continue;
-                float* C = static_cast<float*>(Cv) + int64_t(m) * ldc + nb0 + 4 * g;
+        for (int j = 0; j < 8; ++j) {
+            if (j + 1 < 8) load_block(j + 1, cbuf[(j + 1) & 1]);
+            f32x4 cj[8];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    f32x4* p = reinterpret_cast<f32x4*>(C + 16 * i);
-                    f32x4 v = *p;
-                    v += c[i][h];
-                    *p = v;
-                }
+            for (int i = 0; i < 8; ++i) {
+                asm volatile("" : "+a"(acc[i][j]) : : "memory");
+                cj[i] = acc[i][j];
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                *reinterpret_cast<f32x4*>(stg + lr * 512 + (((4 * i + g) ^ f(lr)) * 16)) = cj[i];
+            f32x4 v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int r = 2 * k + half;
+                v[k] = *reinterpret_cast<const f32x4*>(stg + r * 512 + (((lane & 31) ^ f(r)) * 16));
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int m = mb + 16 * j + 2 * k + half;
+                if (m < M) *reinterpret_cast<f32x4*>(C + int64_t(m) * ldc + col) = v[k] + cbuf[j & 1][k];
             }
         }
+        // Wait for the stores too (and with them, vmcnt being in order, everything before
+        // them), once per tile: otherwise the compiler protects the stores' data registers
+        // with vmcnt waits inside the next K loop, where they would stall behind the loads.
+        __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
         return;
     }
     // bf16 outputs: 128 columns (16 chunks) per row, or 64 (8 chunks) after SwiGLU
