@@ -166,49 +166,98 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
         __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
         return;
     }
-    // bf16 outputs: 128 columns (16 chunks) per row, or 64 (8 chunks) after SwiGLU
-    constexpr int CH = EPI == ppk::kSwiGLU ? 8 : 16;
-    int head = 0, kind = 0;
     if constexpr (EPI == ppk::kQkvRope) {
         // The wavefront's 128 columns are exactly one head (tiles start at multiples of 256),
         // and the rotate-half partners c and c + 64 are accumulator blocks i and i + 4 of the
         // same lane: RoPE is applied to the float32 accumulators before the one rounding.
-        head = nb0 >> 7;
-        kind = head < qo.H ? 0 : (head < qo.H + qo.Hkv ? 1 : 2);   // q, k, v (uniform)
+        // One 16-row block j at a time, staged through LDS (16 rows x 256 bytes) and stored
+        // as whole rows.  The slot metadata of all 8 of the lane's rows is read first; the
+        // cos/sin rows of block j + 1 are requested before block j is stored (vmcnt counts
+        // stores and completes in order).
+        const int head = nb0 >> 7;
+        const int kind = head < qo.H ? 0 : (head < qo.H + qo.Hkv ? 1 : 2);   // q, k, v (uniform)
+        int drow[8], pos[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int m = mb + 16 * j + lr, mc = min(m, M - 1);
+            const int seg = slot_seg[mc], p = qo.slot_pos[mc];
+            const int kv = kind > 0 ? qo.slot_kv[mc] : m;
+            drow[j] = m < M ? kv : -1;
+            pos[j] = seg >= 0 ? p : 0;
+        }
+        f32x4 tb[2][8];
+        auto load_tab = [&](int j, f32x4 (&t)[8]) {
+            const float2* cs = qo.table + int64_t(pos[j]) * 64 + 4 * g;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                t[2 * i] = *reinterpret_cast<const f32x4*>(cs + 16 * i);
+                t[2 * i + 1] = *reinterpret_cast<const f32x4*>(cs + 16 * i + 2);
+            }
+        };
+        if (kind < 2) load_tab(0, tb[0]);
+        bf16* base = kind == 0 ? static_cast<bf16*>(qo.q) + head * 128
+                               : static_cast<bf16*>(kind == 1 ? qo.kc : qo.vc) +
+                                     (head - qo.H - (kind == 2 ? qo.Hkv : 0)) * 128;
+        const int64_t ld = kind == 0 ? qo.ldq : qo.ldkv;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (kind < 2 && j + 1 < 8) load_tab(j + 1, tb[(j + 1) & 1]);
+            f32x4 c[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                asm volatile("" : "+a"(acc[i][j]) : : "memory");
+                c[i] = acc[i][j];
+            }
+            if (kind < 2) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const f32x4 t0 = tb[j & 1][2 * i], t1 = tb[j & 1][2 * i + 1];
+                    const float cv[4] = {t0[0], t0[2], t1[0], t1[2]};
+                    const float sv[4] = {t0[1], t0[3], t1[1], t1[3]};
+                    bf16x4 lo, hi;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float x = c[i][e], y = c[i + 4][e];
+                        lo[e] = static_cast<bf16>(x * cv[e] - y * sv[e]);
+                        hi[e] = static_cast<bf16>(y * cv[e] + x * sv[e]);
+                    }
+                    stage_put<16>(stg, lr, 2 * i + (g >> 1), g & 1, lo);
+                    stage_put<16>(stg, lr, 8 + 2 * i + (g >> 1), g & 1, hi);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    bf16x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(c[i][e]);
+                    stage_put<16>(stg, lr, 2 * i + (g >> 1), g & 1, v);
+                }
+            }
+            bf16x8 v[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int r = 4 * k + lane / 16, ch = lane % 16;
+                v[k] = *reinterpret_cast<const bf16x8*>(stg + r * 256 + ((ch ^ r) * 16));
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int r = 4 * k + lane / 16, ch = lane % 16;
+                const int d = __shfl(drow[j], r);   // lane r holds row r's destination
+                if (d >= 0) *reinterpret_cast<bf16x8*>(base + int64_t(d) * ld + ch * 8) = v[k];
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));   // as in the residual epilogue
+        return;
     }
+    // bf16 outputs: 128 columns (16 chunks) per row, or 64 (8 chunks) after SwiGLU
+    constexpr int CH = EPI == ppk::kSwiGLU ? 8 : 16;
 #pragma unroll
     for (int jp = 0; jp < 4; ++jp) {
         f32x4 c[8][2];
         take_pair(acc, jp, c);
-        int dst_row[2];   // destination rows of this lane's two activation rows (< 0: none)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            const int m = mb + 32 * jp + 16 * h + lr;
             const int r = 16 * h + lr;   // row in the staging block
-            dst_row[h] = m;
-            if constexpr (EPI == ppk::kQkvRope) {
-                if (kind > 0) dst_row[h] = m < M ? qo.slot_kv[m] : -1;
-                if (kind < 2) {
-                    const int pos = m < M && slot_seg[m] >= 0 ? qo.slot_pos[m] : 0;
-                    const float2* cs = qo.table + int64_t(pos) * 64 + 4 * g;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const f32x4 t0 = *reinterpret_cast<const f32x4*>(cs + 16 * i);
-                        const f32x4 t1 = *reinterpret_cast<const f32x4*>(cs + 16 * i + 2);
-                        const float cv[4] = {t0[0], t0[2], t1[0], t1[2]};
-                        const float sv[4] = {t0[1], t0[3], t1[1], t1[3]};
-                        bf16x4 lo, hi;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const float a = c[i][h][e], b = c[i + 4][h][e];
-                            lo[e] = static_cast<bf16>(a * cv[e] - b * sv[e]);
-                            hi[e] = static_cast<bf16>(b * cv[e] + a * sv[e]);
-                        }
-                        stage_put<CH>(stg, r, 2 * i + (g >> 1), g & 1, lo);
-                        stage_put<CH>(stg, r, 8 + 2 * i + (g >> 1), g & 1, hi);
-                    }
-                }
-            }
             if constexpr (EPI == ppk::kSwiGLU) {
                 // weight rows 32 k .. +15 (block 2 k) are gate rows, 32 k + 16 .. +31 (block
                 // 2 k + 1) the matching up rows: output column 16 k + 4 g + e
@@ -219,7 +268,7 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
                     for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(silu_rcp(c[2 * k][h][e]) * c[2 * k + 1][h][e]);
                     stage_put<CH>(stg, r, 2 * k + (g >> 1), g & 1, v);
                 }
-            } else if (EPI == ppk::kStore || kind == 2) {
+            } else {
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
                     bf16x4 v;
@@ -241,20 +290,9 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
         for (int k = 0; k < 32 / RPI; ++k) {
             const int r = k * RPI + lane / CH, ch = lane % CH;
             const int mr = mb + 32 * jp + r;
-            if constexpr (EPI == ppk::kQkvRope) {
-                // lane r % 16 holds row r's destination (in dst_row[r / 16])
-                const int d0 = __shfl(dst_row[0], r & 15), d1 = __shfl(dst_row[1], r & 15);
-                const int drow = r < 16 ? d0 : d1;
-                if (mr >= M || drow < 0) continue;
-                bf16* dst = kind == 0 ? static_cast<bf16*>(qo.q) + int64_t(drow) * qo.ldq + head * 128
-                                      : static_cast<bf16*>(kind == 1 ? qo.kc : qo.vc) + int64_t(drow) * qo.ldkv +
-                                            (head - qo.H - (kind == 2 ? qo.Hkv : 0)) * 128;
-                *reinterpret_cast<bf16x8*>(dst + ch * 8) = v[k];
-            } else {
-                if (mr >= M) continue;
-                bf16* C = static_cast<bf16*>(Cv) + int64_t(mr) * ldc + (EPI == ppk::kSwiGLU ? nb0 / 2 : nb0);
-                *reinterpret_cast<bf16x8*>(C + ch * 8) = v[k];
-            }
+            if (mr >= M) continue;
+            bf16* C = static_cast<bf16*>(Cv) + int64_t(mr) * ldc + (EPI == ppk::kSwiGLU ? nb0 / 2 : nb0);
+            *reinterpret_cast<bf16x8*>(C + ch * 8) = v[k];
         }
     }
     // the staging area is refilled by this wavefront's own loads right after the epilogue
