@@ -20,6 +20,11 @@ positions; Algorithm 1 for the prefill-then-unpack structure):
       cache   = (k after RoPE, v)               the layer's KV cache
   hidden = RMSNorm(x) * g_final
 
+First token (section 2.3: the time to first token covers prefilling the KV
+cache and generating the first token; section 4.3 adds the unpacking): for
+every prompt, the logits of its last token, hidden[last] W_lm^T over the
+vocabulary, and the greedy choice argmax, lowest id on ties (``first_token``).
+
 Readings of the paper (each listed with its reason in the design doc):
 * the score scale is 1/sqrt(D), D the head size (the paper writes the
   single-head form with the model width);
@@ -28,7 +33,8 @@ Readings of the paper (each listed with its reason in the design doc):
 * a query with no allowed key (a pad slot under M') has output 0;
 * the cached K is the post-RoPE K;
 * RoPE angles are formed and evaluated in float64;
-* the final hidden state is taken after the final RMSNorm.
+* the final hidden state is taken after the final RMSNorm;
+* the first token is chosen greedily (the paper names no sampler).
 
 Modes, which the paper asserts give the exact same caches (section 3.3):
 * ``prefill_per_prompt`` -- every prompt alone, causal mask, positions
@@ -262,6 +268,26 @@ def prefill_padded(lengths: Sequence[int], tokens: np.ndarray, weights: Dict, sh
             out.k[layer][a:b] = r.k[layer][:l]
             out.v[layer][a:b] = r.v[layer][:l]
     return out
+
+
+# ----------------------------------------------------------------------------- first token
+def last_token_rows(lengths: Sequence[int]) -> np.ndarray:
+    """Row of each prompt's last token in the unpacked hidden state (original order)."""
+    return np.cumsum(np.asarray(lengths, dtype=np.int64)) - 1
+
+
+def first_token(hidden: np.ndarray, lengths: Sequence[int], lm_head: np.ndarray,
+                rnd: Rounder = _ident):
+    """Greedy first token of every prompt (section 2.3).
+
+    hidden [total_len, d] in original prompt order; lm_head [vocab, d].
+    Returns (logits [k, vocab] float64, tokens [k] int64): logits of prompt i
+    = rnd(hidden[last_i]) . lm_head[v] over v, token = the first v of maximal
+    logit (numpy's argmax takes the first maximum).
+    """
+    h = rnd(np.asarray(hidden, dtype=np.float64)[last_token_rows(lengths)])
+    logits = h @ np.asarray(lm_head, dtype=np.float64).T
+    return logits, np.argmax(logits, axis=1)
 
 
 # ----------------------------------------------------------------------------- bf16 floor

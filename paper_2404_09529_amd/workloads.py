@@ -19,7 +19,7 @@ here, so every workload is synthetic:
 
 Random streams: ``numpy.random.default_rng([workload_id, seed, stream])`` with
 stream 0 = lengths, 1 = tokens, 2 = weights, 3 = norm gains (parity cases only;
-the benchmark workloads use unit gains).
+the benchmark workloads use unit gains), 4 = the LM head (first-token step).
 """
 from __future__ import annotations
 
@@ -205,6 +205,13 @@ def draw_weights(wl: Workload, seed: int, shape: Optional[ModelShape] = None,
     out["layers"] = layers
     out["final_norm"] = gain()
     return out
+
+
+def draw_lm_head(wl: Workload, seed: int, shape: Optional[ModelShape] = None) -> np.ndarray:
+    """The LM head [vocab, d] (float32; bf16-exact values for bf16 shapes), own stream 4."""
+    s = wl.shape if shape is None else shape
+    rng = np.random.default_rng([wl.wid, seed, 4])
+    return _normal(rng, (s.vocab, s.d_model), s.dtype == "bf16")
 
 
 @dataclass

@@ -30,6 +30,19 @@ def build(shape, weights):
     return model
 
 
+def last_logits(shape, weights, lm_head, ids):
+    """Hugging Face's causal LM (LlamaForCausalLM: the decoder, its final norm and the LM
+    head) on one prompt; the float64 logits at the prompt's last position, [vocab]."""
+    from transformers import LlamaForCausalLM
+    base = build(shape, weights)
+    lm = LlamaForCausalLM(base.config).double().eval()
+    lm.model = base
+    lm.lm_head.weight.data = torch.from_numpy(np.asarray(lm_head, dtype=np.float64))
+    with torch.no_grad():
+        out = lm(input_ids=torch.as_tensor(ids, dtype=torch.long)[None])
+    return out.logits[0, -1].numpy()
+
+
 def run(model, ids, attention_mask=None, position_ids=None):
     """Returns (hidden [b, n, d], [K_l [b, n, Hkv*D]], [V_l ...]) as numpy float64."""
     with torch.no_grad():
