@@ -277,6 +277,36 @@ pp_status pp_attention(const pp_config* cfg, const pp_dplan* plan, const void* q
 pp_status pp_final_norm_unpack(const float* x, const float* gain, int32_t d, float eps, const pp_dplan* plan,
                                float* hidden, void* stream);
 
+/* ------------------------------------------------------------------------------------------
+ * First token (section 2.3: the time to first token is the time to prefill the KV cache and
+ * generate the first token; section 4.3 adds the unpacking, which pp_prefill already did).
+ * ---------------------------------------------------------------------------------------- */
+
+/* Bytes of device workspace pp_first_token needs for this config and plan.
+ * Errors: PP_ERR_INVALID_ARG, PP_ERR_UNSUPPORTED (as pp_prefill). */
+pp_status pp_first_token_workspace_size(const pp_config* cfg, const pp_dplan* plan, size_t* bytes);
+
+/* Greedy first token of every prompt of the plan: for prompt i (original order), its last
+ * token's hidden row h_i = hidden[prompt_kv_off[i+1] - 1], the logits h_i . lm_head[v] for
+ * every v < vocab, and tokens[i] = the v of maximal logit, the lowest v on ties (-1 if every
+ * logit is NaN; NaN logits are never chosen).
+ *
+ *   hidden    device float32 [total_len, d]: pp_prefill's output
+ *   lm_head   device [vocab, d] in the config dtype, row-major ([out, in])
+ *   workspace device, >= pp_first_token_workspace_size bytes, 256-byte aligned
+ *   logits    device float32 [k, vocab], or NULL when not wanted
+ *   tokens    device int32 [k]
+ *   stream    a hipStream_t (NULL = the default stream)
+ *
+ * Numerics: PP_BF16 rounds h_i to bf16 (as every projection input of the bf16 model) and
+ * accumulates in float32; PP_F32 is float32 throughout.  The argmax is taken on the float32
+ * logits.  Asynchronous; validated before enqueuing; deterministic.
+ * Errors: PP_ERR_INVALID_ARG (NULL pointer, misaligned workspace, inconsistent plan or
+ *         config), PP_ERR_BUFFER_TOO_SMALL (workspace), PP_ERR_UNSUPPORTED (as pp_prefill),
+ *         PP_ERR_HIP (launch failure). */
+pp_status pp_first_token(const pp_config* cfg, const pp_dplan* plan, const float* hidden, const void* lm_head,
+                         void* workspace, size_t workspace_bytes, float* logits, int32_t* tokens, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -83,4 +83,13 @@ void attention_f32(const float* q, int64_t ldq, const float* kc, const float* vc
                    int64_t ldo, const int32_t* slot_seg, const int32_t* seg_prompt, const int32_t* seg_start,
                    const int32_t* prompt_kv_off, int T, int H, int Hkv, int D, hipStream_t s);
 
+// First token (greedy) of each of k prompts: logits[m][v] = hidden[prompt_kv_off[m+1]-1] .
+// lm_head[v] (hidden row rounded to dtype; float32 accumulation), tokens[m] = argmax over v,
+// lowest v on ties, -1 if every logit is NaN.  lm_head [V, d] in dtype; logits [k, V] float32
+// or null; workspace of first_token_workspace(dtype, k, V, d) bytes, 256-byte aligned.
+// bf16: d % 128 == 0.
+size_t first_token_workspace(int dtype, int k, int V, int d);
+void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, int k, const void* lm_head, int V,
+                 int d, void* workspace, float* logits, int32_t* tokens, hipStream_t s);
+
 }  // namespace ppk

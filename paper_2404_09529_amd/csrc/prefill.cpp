@@ -391,3 +391,34 @@ extern "C" pp_status pp_final_norm_unpack(const float* x, const float* gain, int
     ppk::rmsnorm_unpack(x, gain, hidden, plan->slot_kv, T, d, eps, static_cast<hipStream_t>(stream));
     return finish("final_norm_unpack");
 }
+
+extern "C" pp_status pp_first_token_workspace_size(const pp_config* cfg, const pp_dplan* plan, size_t* bytes) {
+    pp::clear_error();
+    if (pp_status st = validate_config(cfg)) return st;
+    if (pp_status st = validate_plan(plan)) return st;
+    if (!bytes) return pp::fail(PP_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = plan->k > 0 ? ppk::first_token_workspace(cfg->dtype, plan->k, cfg->vocab, cfg->d_model) : 0;
+    return PP_OK;
+}
+
+extern "C" pp_status pp_first_token(const pp_config* cfg, const pp_dplan* plan, const float* hidden,
+                                    const void* lm_head, void* workspace, size_t workspace_bytes, float* logits,
+                                    int32_t* tokens, void* stream) {
+    pp::clear_error();
+    if (pp_status st = validate_config(cfg)) return st;
+    if (pp_status st = validate_plan(plan)) return st;
+    if (plan->k == 0) return PP_OK;
+    if (plan->total_len < plan->k)
+        return pp::fail(PP_ERR_INVALID_ARG, "plan has %d prompts but %d tokens", plan->k, plan->total_len);
+    if (!plan->prompt_kv_off) return pp::fail(PP_ERR_INVALID_ARG, "prompt_kv_off is NULL");
+    if (!hidden || !lm_head || !tokens || !workspace) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+        return pp::fail(PP_ERR_INVALID_ARG, "workspace is not %zu-byte aligned", kAlign);
+    const size_t need = ppk::first_token_workspace(cfg->dtype, plan->k, cfg->vocab, cfg->d_model);
+    if (workspace_bytes < need)
+        return pp::fail(PP_ERR_BUFFER_TOO_SMALL, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
+    (void)hipGetLastError();
+    ppk::first_token(cfg->dtype, hidden, plan->prompt_kv_off, plan->k, lm_head, cfg->vocab, cfg->d_model, workspace,
+                     logits, tokens, static_cast<hipStream_t>(stream));
+    return finish("first_token");
+}

@@ -99,9 +99,11 @@ def lib() -> ctypes.CDLL:
         L.pp_attention.argtypes = [cfgp, dpp, vp, i64, vp, vp, vp, vp]
         L.pp_qkv_projection.argtypes = [cfgp, dpp, vp, vp, vp, vp, vp, vp, vp]
         L.pp_final_norm_unpack.argtypes = [vp, vp, i32, f32, dpp, vp, vp]
+        L.pp_first_token_workspace_size.argtypes = [cfgp, dpp, ctypes.POINTER(ctypes.c_size_t)]
+        L.pp_first_token.argtypes = [cfgp, dpp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp]
         for name in ("pp_plan_bounds", "pp_pack", "pp_pack_padded", "pp_prefill_workspace_size", "pp_prefill",
                      "pp_embed", "pp_rmsnorm", "pp_gemm", "pp_rope", "pp_kv_scatter", "pp_attention",
-                     "pp_final_norm_unpack"):
+                     "pp_final_norm_unpack", "pp_first_token_workspace_size", "pp_first_token"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -353,3 +355,19 @@ def pp_attention(cfg: PPConfig, dplan: DevicePlan, q, ldq: int, k_cache, v_cache
 def pp_final_norm_unpack(x, gain, d: int, eps: float, dplan: DevicePlan, hidden, stream=None) -> None:
     _check(lib().pp_final_norm_unpack(_p(x), _p(gain), d, eps, ctypes.byref(dplan.struct), _p(hidden),
                                       _stream(stream)), "pp_final_norm_unpack")
+
+
+def pp_first_token_workspace_size(cfg: PPConfig, dplan: DevicePlan) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().pp_first_token_workspace_size(ctypes.byref(cfg), ctypes.byref(dplan.struct), ctypes.byref(n)),
+           "pp_first_token_workspace_size")
+    return n.value
+
+
+def pp_first_token(cfg: PPConfig, dplan: DevicePlan, hidden, lm_head, workspace, tokens, logits=None,
+                   stream=None) -> None:
+    """Greedy first token of every prompt: tokens [k] int32 (and logits [k, vocab] float32)."""
+    _check(lib().pp_first_token(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(hidden), _p(lm_head),
+                                _p(workspace), workspace.numel() * workspace.element_size(), _p(logits),
+                                _p(tokens), _stream(stream)), "pp_first_token")
+

@@ -235,3 +235,26 @@ def test_gemm_rejects_unsupported_shapes_before_enqueue(L):
     assert call(lda=100) == pp.PP_ERR_INVALID_ARG          # lda < K
     assert call(M=0) == pp.PP_OK                           # empty: nothing to do
     assert g(pp.PP_BF16, 7, 0x1000, 4096, 0x2000, 4096, 0x3000, 4096, 256, 4096, 4096, None, None) == pp.PP_ERR_INVALID_ARG
+
+
+def test_first_token_workspace_and_rejections(L):
+    """Workspace size of the first-token step, and its host-side argument checks."""
+    cfg, dp = _cfg(vocab=32000), _dplan()
+    n = ctypes.c_size_t()
+    assert L.pp_first_token_workspace_size(ctypes.byref(cfg), ctypes.byref(dp), ctypes.byref(n)) == pp.PP_OK
+    # k = 2 prompts padded to 16 rows of d bf16, then one (float, int32) pair per 64-row block and prompt
+    assert n.value == 16 * 4096 * 2 + 500 * 2 * 8
+    ws = n.value
+    f = L.pp_first_token
+    ok = dict(h=0x1000, w=0x2000, ws=0x10000, nb=ws, lg=None, tok=0x3000)
+    def call(c=cfg, p=dp, **kw):
+        a = {**ok, **kw}
+        return f(ctypes.byref(c), ctypes.byref(p), a["h"], a["w"], a["ws"], a["nb"], a["lg"], a["tok"], None)
+    assert call(h=None) == pp.PP_ERR_INVALID_ARG
+    assert call(w=None) == pp.PP_ERR_INVALID_ARG
+    assert call(tok=None) == pp.PP_ERR_INVALID_ARG
+    assert call(ws=0x10010) == pp.PP_ERR_INVALID_ARG              # not 256-byte aligned
+    assert call(nb=ws - 1) == pp.PP_ERR_BUFFER_TOO_SMALL
+    assert call(p=_dplan(total_len=1)) == pp.PP_ERR_INVALID_ARG   # fewer tokens than prompts
+    assert call(c=_cfg(vocab=0)) == pp.PP_ERR_INVALID_ARG
+    assert call(p=_dplan(k=0, total_len=0)) == pp.PP_OK            # no prompt: nothing to do
