@@ -30,6 +30,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 METRIC = "effective prefill tokens/s + TFLOP/s (% bf16 MFMA peak) vs padded prefill"
 GEMM_SOURCE = os.path.join(ROOT, "paper_2404_09529_amd", "csrc", "k_gemm_bf16.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_swiglu_llama2-7b-lognormal_traffic.md")
@@ -263,7 +264,27 @@ def main():
                      "algorithmic_flop_per_launch": k_flops, "algorithmic_bytes_per_launch": k_bytes,
                      "traffic_source": None if traffic is None else os.path.relpath(TRAFFIC_SUMMARY, ROOT)},
     }
-    del step
+
+    # time to first token (section 2.3): the prefill step plus the greedy first token of every
+    # prompt (LM head on its last token, argmax); the LM head streams 2 V d bytes from HBM
+    V = shape.vocab
+    lm_head = torch.from_numpy(W.draw_lm_head(case.wl, args.seed, shape)).cuda().to(model.torch_dtype)
+    cfg = pp.config_of(shape)
+    ft_ws = torch.empty(pp.pp_first_token_workspace_size(cfg, dplan), dtype=torch.uint8, device="cuda")
+    first = torch.empty(len(lengths), dtype=torch.int32, device="cuda")
+    ftok = lambda: pp.pp_first_token(cfg, dplan, step.hidden, lm_head, ft_ws, first, None, kstream)
+    ft = time_steps(ftok, args.kernel_launches, 3)
+    both = time_steps(lambda: (step(tokens, kstream), ftok()), args.steps, args.warmup)
+    lm_bytes = lm_head.numel() * lm_head.element_size()
+    out["ttft"] = {"ms_median": round(both["ms_median"], 4), "ms_mean": round(both["ms_mean"], 4),
+                   "first_token_ms": round(ft["ms_mean"], 4), "prefill_ms_median": round(packed["ms_median"], 4),
+                   "first_token_roofline": {"bound": "hbm", "achieved": round(lm_bytes / (ft["ms_mean"] / 1e3) / 1e9, 1),
+                                            "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                                            "frac": round(lm_bytes / (ft["ms_mean"] / 1e3) / 1e9 / PEAK_HBM_GBPS, 4),
+                                            "algorithmic_bytes_per_launch": lm_bytes, "vocab": V}}
+    log(f"first token: {ft['ms_mean'] * 1e3:.1f} us ({lm_bytes / (ft['ms_mean'] / 1e3) / 1e9:.0f} GB/s on the LM head); "
+        f"TTFT {both['ms_median']:.3f} ms")
+    del step, lm_head, ft_ws
     torch.cuda.empty_cache()
 
     if not args.no_padded:

@@ -5,7 +5,7 @@
 //
 // Three launches.  (1) The last hidden row of every prompt (row prompt_kv_off[i+1] - 1 of the
 // unpacked hidden state) is gathered into a [k_pad, d] matrix in the model's dtype, rows past
-// k zero.  (2) One workgroup per 64 vocabulary rows computes their logits for all prompts and
+// k zero.  (2) One workgroup per 128 vocabulary rows computes their logits for all prompts and
 // reduces them to one (max, lowest id) pair per prompt.  The LM head, vocab x d, is read from
 // HBM exactly once and dominates the traffic: this kernel is HBM-bound on it (2 vocab d bytes
 // in bf16), the prompt matrix being re-read from L2.  (3) One thread per prompt reduces the
@@ -18,7 +18,7 @@
 
 namespace {
 
-constexpr int VB = 64;   // vocabulary rows per workgroup (4 wavefronts x 16)
+constexpr int VB = 64;   // vocabulary rows per workgroup of the float32 kernel
 
 struct ArgMax {
     float v;
@@ -44,53 +44,123 @@ __global__ __launch_bounds__(256) void gather_last_kernel(const float* __restric
     for (int c = threadIdx.x; c < d; c += blockDim.x) o[c] = static_cast<T>(h[c]);
 }
 
-// Wavefront w of workgroup b owns vocabulary rows n0 = 64 b + 16 w .. + 15 as the first
-// operand of the 16x16x32 bf16 MFMA (weight rows on the MFMA's rows) and all prompts, 64 at a
-// time (4 blocks of 16), as the second.  Fragments come straight from global memory: lane l
-// reads 8 consecutive K values of row l % 16 at K offset 8 (l / 16), so four lanes cover 64
-// contiguous bytes of a row.  Rows past the vocabulary are read as the last row and never
-// reported.  In block mb lane l holds the logits of prompt 16 mb + l % 16 for vocabulary rows
-// n0 + 4 (l / 16) + 0..3.
+// Wavefront w of workgroup b owns vocabulary rows n0 = 128 b + 32 w .. + 31 (two blocks of
+// 16 on the rows of the 16x16x32 bf16 MFMA) and all prompts, 64 at a time (4 blocks of 16 on
+// its columns).  The weight rows stream from HBM straight into registers: lane l reads 8
+// consecutive K values of row l % 16 at K offset 8 (l / 16) of a 32-wide step, and the
+// fragments of step t + 8 are requested while step t is computed (a ring of 8 steps, 16 KB
+// per wavefront in flight).  Rows past the vocabulary are read as the last row and never
+// reported.  The prompt rows are shared by the 4 wavefronts through LDS, 128 K columns at a
+// time, double-buffered: each 128-column tile is read from L2 once per workgroup.  In block
+// (nb, mb) lane l holds the logits of prompt 16 mb + l % 16 for vocabulary rows
+// n0 + 16 nb + 4 (l / 16) + 0..3.
+constexpr int LM_ROWS = 128;        // vocabulary rows per workgroup
+constexpr int HT = 128;             // K columns per LDS tile of prompt rows
+constexpr int HT_B = 64 * HT * 2;   // one tile: 64 prompt rows x 256 bytes
+
+// LDS swizzle of the prompt tile: row r's 16-byte chunk q sits at q ^ g(r), g built from r's
+// bits 0, 1, 2 placed at bits 0, 2, 3.  A fragment read serves lanes i and i + 32 together:
+// rows r..r+7 at chunks q and q ^ 2; a 256-byte row spans all 64 banks, so those 16 accesses
+// are conflict-free when the g(r) fall in distinct classes {x, x ^ 2}, which this g does.
+__device__ __forceinline__ int gsw(int r) { return (r & 1) | (((r >> 1) & 1) << 2) | (((r >> 2) & 1) << 3); }
+
 __global__ __launch_bounds__(256) void lm_head_bf16_kernel(const bf16* __restrict__ hl, int k, int k_pad,
                                                            const bf16* __restrict__ W, int V, int d,
                                                            float* __restrict__ logits, ArgMax* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) char tile[2][HT_B];
     __shared__ ArgMax red[4][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n0 = blockIdx.x * VB + wave * 16;
-    const int lr = lane & 15, kq = 8 * (lane >> 4);
-    const bf16* wrow = W + int64_t(min(n0 + lr, V - 1)) * d + kq;
+    const int n0 = blockIdx.x * LM_ROWS + wave * 32;
+    const int lr = lane & 15, q4 = lane >> 4;
+    const bf16* wrow[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) wrow[nb] = W + int64_t(min(n0 + 16 * nb + lr, V - 1)) * d + 8 * q4;
+    const int S = d / 32;               // K steps of 32; d % 256 == 0, so S % 8 == 0
+    const int n_tiles = d / HT;
+    // prompt-tile loads: load t (0..3) of wavefront w covers rows 4 (4 w + t) + l / 16, chunk l % 16
+    int h_row[4], h_lds[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        h_row[t] = 4 * (4 * wave + t) + q4;
+        h_lds[t] = h_row[t] * 256 + 16 * (lr ^ gsw(h_row[t] & 7));
+    }
+    // fragment reads: row 16 mb + lr, chunk 4 s + q4 (s = step within the tile)
+    const int f_base = lr * 256;
+    const int f_sw = gsw(lr & 7);
     for (int m0 = 0; m0 < k_pad; m0 += 64) {
         const int nmb = min(4, (k_pad - m0) / 16);
-        f32x4 acc[4] = {};
-        const bf16* hrow = hl + int64_t(m0 + lr) * d + kq;
-        for (int kk = 0; kk < d; kk += 128) {
-            // the 4 weight fragments of this 128-wide slice first: they come from HBM
-            bf16x8 w[4];
+        bf16x8 hreg[4];
+        auto load_tile = [&](int c) {   // prompt rows m0.., K columns c*HT.. (clamped: always in range)
+            const int cc = min(c, n_tiles - 1);
 #pragma unroll
-            for (int s = 0; s < 4; ++s) w[s] = *reinterpret_cast<const bf16x8*>(wrow + kk + 32 * s);
+            for (int t = 0; t < 4; ++t) {
+                const int row = min(m0 + h_row[t], k_pad - 1);
+                hreg[t] = *reinterpret_cast<const bf16x8*>(hl + int64_t(row) * d + cc * HT + lr * 8);
+            }
+        };
+        auto store_tile = [&](int buf) {
 #pragma unroll
-            for (int s = 0; s < 4; ++s)
+            for (int t = 0; t < 4; ++t) *reinterpret_cast<bf16x8*>(tile[buf] + h_lds[t]) = hreg[t];
+        };
+        bf16x8 ring[8][2];
+        auto load_w = [&](int u, int t) {   // weight fragments of step t (clamped) into ring slot u
+            const int tt = min(t, S - 1);
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb)
-                    if (mb < nmb) {
-                        const bf16x8 h = *reinterpret_cast<const bf16x8*>(hrow + int64_t(16 * mb) * d + kk + 32 * s);
-                        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[s], h, acc[mb], 0, 0, 0);
-                    }
+            for (int nb = 0; nb < 2; ++nb) ring[u][nb] = *reinterpret_cast<const bf16x8*>(wrow[nb] + 32 * tt);
+        };
+        f32x4 acc[2][4] = {};
+        auto step = [&](int u, int buf, int s) {   // compute ring slot u with tile buf, step s of it
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) {
+                if (mb >= nmb) break;
+                const bf16x8 h = *reinterpret_cast<const bf16x8*>(
+                    tile[buf] + f_base + 16 * mb * 256 + 16 * ((4 * s + q4) ^ f_sw));
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb)
+                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[u][nb], h, acc[nb][mb], 0, 0, 0);
+            }
+        };
+        load_tile(0);
+        store_tile(0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) load_w(u, u);
+        __syncthreads();
+        for (int t0 = 0; t0 < S; t0 += 8) {
+            const int c = t0 / 4;   // tiles c (buffer 0) and c + 1 (buffer 1)
+            load_tile(c + 1);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                step(u, 0, u);
+                load_w(u, t0 + 8 + u);
+            }
+            store_tile(1);
+            __syncthreads();
+            load_tile(c + 2);
+#pragma unroll
+            for (int u = 4; u < 8; ++u) {
+                step(u, 1, u - 4);
+                load_w(u, t0 + 8 + u);
+            }
+            store_tile(0);
+            __syncthreads();
         }
-        // logits and the lane's best of its 4 vocabulary rows, per prompt block
+        // logits and each lane's best of its 8 vocabulary rows, per prompt block
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb) {
             if (mb >= nmb) break;
             const int m = m0 + 16 * mb + lr;
-            const int nb = n0 + 4 * (lane >> 4);
             float bv = -INFINITY;
             int bi = INT32_MAX;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                if (nb + r >= V) continue;
-                const float v = acc[mb][r];
-                if (logits && m < k) logits[int64_t(m) * V + nb + r] = v;
-                if (better(v, nb + r, bv, bi)) { bv = v; bi = nb + r; }
+            for (int nb = 0; nb < 2; ++nb) {
+                const int nbase = n0 + 16 * nb + 4 * q4;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if (nbase + r >= V) continue;
+                    const float v = acc[nb][mb][r];
+                    if (logits && m < k) logits[int64_t(m) * V + nbase + r] = v;
+                    if (better(v, nbase + r, bv, bi)) { bv = v; bi = nbase + r; }
+                }
             }
             // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same prompt
 #pragma unroll
@@ -102,7 +172,7 @@ __global__ __launch_bounds__(256) void lm_head_bf16_kernel(const bf16* __restric
             if (lane < 16) red[wave][16 * mb + lane] = ArgMax{bv, bi};
         }
         __syncthreads();
-        // wavefront 0 combines the 4 wavefronts' rows (ascending ids) for the 64 prompts
+        // wavefront 0 combines the 4 wavefronts' rows for the 64 prompts
         if (wave == 0 && lane < 16 * nmb && m0 + lane < k) {
             ArgMax b = red[0][lane];
 #pragma unroll
@@ -163,7 +233,8 @@ size_t first_token_workspace(int dtype, int k, int V, int d) {
     const int k_pad = (k + 15) / 16 * 16;
     const size_t e = dtype == PP_BF16 ? 2 : 4;
     const size_t a = (size_t(k_pad) * d * e + 255) / 256 * 256;
-    const size_t n_blocks = (size_t(V) + VB - 1) / VB;
+    const size_t rows = dtype == PP_BF16 ? LM_ROWS : VB;
+    const size_t n_blocks = (size_t(V) + rows - 1) / rows;
     return a + n_blocks * size_t(k) * sizeof(ArgMax);
 }
 
@@ -173,7 +244,7 @@ void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, i
     const size_t e = dtype == PP_BF16 ? 2 : 4;
     char* ws = static_cast<char*>(workspace);
     ArgMax* part = reinterpret_cast<ArgMax*>(ws + (size_t(k_pad) * d * e + 255) / 256 * 256);
-    const int n_blocks = (V + VB - 1) / VB;
+    const int n_blocks = (V + (dtype == PP_BF16 ? LM_ROWS : VB) - 1) / (dtype == PP_BF16 ? LM_ROWS : VB);
     if (dtype == PP_BF16) {
         bf16* hl = reinterpret_cast<bf16*>(ws);
         gather_last_kernel<bf16><<<k_pad, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);

@@ -242,8 +242,9 @@ def test_first_token_workspace_and_rejections(L):
     cfg, dp = _cfg(vocab=32000), _dplan()
     n = ctypes.c_size_t()
     assert L.pp_first_token_workspace_size(ctypes.byref(cfg), ctypes.byref(dp), ctypes.byref(n)) == pp.PP_OK
-    # k = 2 prompts padded to 16 rows of d bf16, then one (float, int32) pair per 64-row block and prompt
-    assert n.value == 16 * 4096 * 2 + 500 * 2 * 8
+    # k = 2 prompts padded to 16 rows of d bf16, then one (float, int32) pair per 128-row
+    # vocabulary block and prompt
+    assert n.value == 16 * 4096 * 2 + 250 * 2 * 8
     ws = n.value
     f = L.pp_first_token
     ok = dict(h=0x1000, w=0x2000, ws=0x10000, nb=ws, lg=None, tok=0x3000)
