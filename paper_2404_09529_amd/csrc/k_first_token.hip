@@ -8,8 +8,8 @@
 // k zero.  (2) One workgroup per 128 vocabulary rows computes their logits for all prompts and
 // reduces them to one (max, lowest id) pair per prompt.  The LM head, vocab x d, is read from
 // HBM exactly once and dominates the traffic: this kernel is HBM-bound on it (2 vocab d bytes
-// in bf16), the prompt matrix being re-read from L2.  (3) One thread per prompt reduces the
-// per-workgroup pairs in workgroup order, so the result is deterministic.
+// in bf16), the prompt matrix being re-read from L2.  (3) One workgroup per prompt reduces the
+// per-workgroup pairs; the order it uses is total, so the result is deterministic.
 #include <math.h>
 
 #include "device.h"
@@ -213,16 +213,33 @@ __global__ __launch_bounds__(VB) void lm_head_f32_kernel(const float* __restrict
     }
 }
 
+// One workgroup per prompt: thread t takes the per-workgroup pairs t, t + 256, ..., then the
+// pairs are combined across the wavefront and across the 4 wavefronts.  "Larger value, then
+// lower id" is a total order on the pairs (NaN never enters one), so the result does not
+// depend on the order of combination.
 __global__ __launch_bounds__(256) void argmax_finalize_kernel(const ArgMax* __restrict__ part, int n_blocks, int k,
                                                               int32_t* __restrict__ tokens) {
-    const int m = blockIdx.x * blockDim.x + threadIdx.x;
-    if (m >= k) return;
+    __shared__ ArgMax red[4];
+    const int m = blockIdx.x;
     ArgMax b{-INFINITY, INT32_MAX};
-    for (int j = 0; j < n_blocks; ++j) {
+    for (int j = threadIdx.x; j < n_blocks; j += blockDim.x) {
         const ArgMax o = part[int64_t(j) * k + m];
         if (better(o.v, o.i, b.v, b.i)) b = o;
     }
-    tokens[m] = b.i == INT32_MAX ? -1 : b.i;   // -1: every logit was NaN
+#pragma unroll
+    for (int x = 1; x < 64; x <<= 1) {
+        const float ov = __shfl_xor(b.v, x);
+        const int oi = __shfl_xor(b.i, x);
+        if (better(ov, oi, b.v, b.i)) b = ArgMax{ov, oi};
+    }
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = b;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int w = 1; w < 4; ++w)
+            if (better(red[w].v, red[w].i, b.v, b.i)) b = red[w];
+        tokens[m] = b.i == INT32_MAX ? -1 : b.i;   // -1: every logit was NaN
+    }
 }
 
 }  // namespace
@@ -255,7 +272,7 @@ void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, i
         gather_last_kernel<float><<<k_pad, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);
         lm_head_f32_kernel<<<n_blocks, VB, 0, s>>>(hl, k, static_cast<const float*>(lm_head), V, d, logits, part);
     }
-    argmax_finalize_kernel<<<(k + 255) / 256, 256, 0, s>>>(part, n_blocks, k, tokens);
+    argmax_finalize_kernel<<<k, 256, 0, s>>>(part, n_blocks, k, tokens);
 }
 
 }  // namespace ppk
