@@ -160,6 +160,229 @@ def cpu_baseline(case, budget_s):
                       f"{el:.1f} s"}
 
 
+# ----------------------------------------------------------------------------- sweeps
+def batch_predictors(lengths, n_rows):
+    """The two batch statistics the paper regresses the speedup on (section 4.6): the batch-size
+    reduction r/k (packed rows over prompts) and the max absolute deviation m - L/k (the longest
+    prompt minus the mean length)."""
+    import numpy as np
+    lengths = np.asarray(lengths, dtype=np.int64)
+    k = len(lengths)
+    return {"r_over_k": n_rows / k, "max_abs_dev": float(lengths.max() - lengths.sum() / k)}
+
+
+def linear_fit(x, y):
+    """Ordinary least squares y ~ a + b x: slope b, intercept a, Pearson correlation and R^2."""
+    import numpy as np
+    x, y = np.asarray(x, dtype=np.float64), np.asarray(y, dtype=np.float64)
+    xm, ym = x.mean(), y.mean()
+    sxx, syy, sxy = np.sum((x - xm) ** 2), np.sum((y - ym) ** 2), np.sum((x - xm) * (y - ym))
+    b = sxy / sxx
+    r = sxy / np.sqrt(sxx * syy)
+    return {"slope": float(b), "intercept": float(ym - b * xm), "pearson_r": float(r), "r2": float(r * r),
+            "n": int(len(x))}
+
+
+def device_weights(shape, seed):
+    """Random-init weights drawn on the device with torch (N(0, 0.02^2), bf16; unit norm gains)
+    for timing-only sweeps at full model depth, where drawing them on the host would take
+    minutes.  Nothing compares these values with anything."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    s, dt = shape, torch.bfloat16
+
+    def n(*sz):
+        return (torch.randn(sz, generator=g, device="cuda") * 0.02).to(dt)
+
+    ones = lambda: torch.ones(s.d_model, dtype=torch.float32, device="cuda")
+    d, H, Hkv, D, F = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim, s.ffn_dim
+    layers = [dict(wq=n(H * D, d), wk=n(Hkv * D, d), wv=n(Hkv * D, d), wo=n(d, H * D), wg=n(F, d), wu=n(F, d),
+                   wd=n(d, F), attn_norm=ones(), mlp_norm=ones()) for _ in range(s.n_layers)]
+    return {"embed": n(s.vocab, d), "final_norm": ones(), "layers": layers}
+
+
+def time_plan(pp, model, plan, tokens, reps, warmup, lm_head=None):
+    """Median of `reps` timed pp_prefill steps of one plan after `warmup` untimed ones; with an
+    LM head also the time to first token, prefill and pp_first_token timed together."""
+    import torch
+    dplan = pp.DevicePlan(plan)
+    step = pp.Prefill(model, dplan)
+    out = {"ms": time_steps(lambda: step(tokens), reps, warmup)["ms_median"]}
+    if lm_head is not None:
+        cfg = model.config
+        ws = torch.empty(max(pp.pp_first_token_workspace_size(cfg, dplan), 1), dtype=torch.uint8, device="cuda")
+        first = torch.empty(max(plan.k, 1), dtype=torch.int32, device="cuda")
+        out["ttft_ms"] = time_steps(lambda: (step(tokens), pp.pp_first_token(cfg, dplan, step.hidden, lm_head, ws,
+                                                                             first)), reps, warmup)["ms_median"]
+    return out
+
+
+def measure_batch(pp, model, lengths, args, gen, lm_head=None):
+    """One batch prefilled packed (FFD, bin size = the batch's maximum length) and fully
+    batched (every prompt right-padded to that maximum): same kernels, same stream."""
+    import torch
+    shape = model.shape
+    L = int(lengths.sum())
+    tokens = torch.randint(0, shape.vocab, (L,), generator=gen, device="cuda", dtype=torch.int32)
+    plan, pplan = pp.pp_pack(lengths, 0), pp.pp_pack_padded(lengths)
+    rec = {"k": int(len(lengths)), "L": L, "m": int(lengths.max()), "r": plan.n_rows,
+           **batch_predictors(lengths, plan.n_rows)}
+    for name, pl in (("packed", plan), ("padded", pplan)):
+        t = time_plan(pp, model, pl, tokens, args.reps, args.sweep_warmup, lm_head)
+        rec[f"ms_{name}"] = t["ms"]
+        if "ttft_ms" in t:
+            rec[f"ttft_ms_{name}"] = t["ttft_ms"]
+        rec[f"slots_{name}"] = pl.n_slots
+    rec["speedup"] = rec["ms_padded"] / rec["ms_packed"]
+    if lm_head is not None:
+        rec["ttft_speedup"] = rec["ttft_ms_padded"] / rec["ttft_ms_packed"]
+    rec["tflops_packed"] = algorithmic_flops(shape, lengths) / (rec["ms_packed"] / 1e3) / 1e12
+    return rec
+
+
+def sweep_pool(W, name, seed, n):
+    """Prompt lengths of a sweep: the U[1,512] pool or a dataset stand-in, in draw order."""
+    wid = 6 if name == "uniform" else W.DATASETS[name][0]
+    return W.draw_lengths(W.workload(wid), seed)[:n]
+
+
+def dataset_batches(pp, lengths, bs):
+    """The four ways of batching a whole prompt set that the paper compares (section 4.5), as
+    lists of (prompt ids, plan):
+      full       batches of bs prompts in arrival (draw) order, right-padded to the batch maximum;
+      batch      the same batches, each packed on its own (FFD, bin size = the batch maximum);
+      ordered    prompts sorted by length, consecutive batches of bs, right-padded (length-ordered
+                 batching: needs the whole set in advance);
+      dataset    the whole set packed at once (FFD, bin size = the set's maximum), its rows taken
+                 bs at a time (dataset prepacking: also needs the whole set).
+    For `dataset`, FFD run again on the prompts of a group of rows of the whole-set packing (in
+    their original order, same bin size) rebuilds exactly those rows, because every prompt still
+    finds the same first row with room; the row count is checked."""
+    import numpy as np
+    lengths = np.asarray(lengths, dtype=np.int32)
+    n = len(lengths)
+    out = {"full": [], "batch": [], "ordered": [], "dataset": []}
+    for b in range(0, n, bs):
+        ids = np.arange(b, min(b + bs, n))
+        out["full"].append((ids, pp.pp_pack_padded(lengths[ids])))
+        out["batch"].append((ids, pp.pp_pack(lengths[ids], 0)))
+    order = np.argsort(lengths, kind="stable")
+    for b in range(0, n, bs):
+        ids = order[b:b + bs]
+        out["ordered"].append((ids, pp.pp_pack_padded(lengths[ids])))
+    whole = pp.pp_pack(lengths, 0)
+    C = whole.capacity
+    for r0 in range(0, whole.n_rows, bs):
+        r1 = min(r0 + bs, whole.n_rows)
+        ids = np.sort(whole.seg_prompt[whole.row_seg_ptr[r0]:whole.row_seg_ptr[r1]])
+        plan = pp.pp_pack(lengths[ids], C)
+        if plan.n_rows != r1 - r0:
+            raise RuntimeError(f"rows {r0}..{r1} of the whole-set packing rebuilt as {plan.n_rows} rows")
+        out["dataset"].append((ids, plan))
+    return out
+
+
+def run_dataset_packing(pp, W, model, args, gen, out):
+    """Per-prompt prefill time of the four batchings of each prompt set (section 4.5)."""
+    import numpy as np
+    import torch
+    shape = model.shape
+    for name in args.pools.split(","):
+        lengths = sweep_pool(W, name, args.seed, args.prompts)
+        tokens_all = torch.randint(0, shape.vocab, (int(lengths.sum()),), generator=gen, device="cuda",
+                                   dtype=torch.int32)
+        off = np.concatenate([[0], np.cumsum(lengths)])
+        entry = {"pool": name, "prompts": int(len(lengths)), "min": int(lengths.min()),
+                 "mean": float(lengths.mean()), "max": int(lengths.max()), "batch_size": args.batch}
+        for method, batches in dataset_batches(pp, lengths, args.batch).items():
+            total, slots, rows = 0.0, 0, 0
+            for ids, plan in batches:
+                tokens = torch.cat([tokens_all[off[i]:off[i + 1]] for i in ids.tolist()])
+                total += time_plan(pp, model, plan, tokens, args.reps, args.sweep_warmup)["ms"]
+                slots, rows = slots + plan.n_slots, rows + plan.n_rows
+                torch.cuda.empty_cache()
+            entry[method] = {"batches": len(batches), "ms_total": total, "ms_per_prompt": total / len(lengths),
+                             "rows": rows, "slots": slots, "fill": float(lengths.sum()) / slots}
+            log(f"  {name} {method}: {len(batches)} batches, {total:.1f} ms, {total / len(lengths):.4f} ms/prompt, "
+                f"fill {entry[method]['fill']:.3f}")
+        out["pools"].append(entry)
+
+
+def run_sweep(args):
+    """--sweep regression: batches of --batch prompts from the prompt pool, the speedup of
+    packing over full batching per batch, and the linear fits of the speedup on r/k and on
+    m - L/k.  --sweep batch: the mean speedup at each of --batch-sizes.  --sweep datasets: the
+    prefill time and time to first token per batch of --batch prompts, packed and fully
+    batched, over each pool of --pools.  --sweep dataset-packing: per-prompt prefill time of
+    full batching, per-batch packing, length-ordered batching and whole-set packing."""
+    import numpy as np
+    import torch
+
+    from paper_2404_09529_amd import prepack as pp
+    from paper_2404_09529_amd import workloads as W
+
+    shape = W.MODELS[args.model]
+    if args.layers:
+        shape = shape.replace(n_layers=args.layers)
+    t = time.perf_counter()
+    model = pp.DeviceModel(shape, device_weights(shape, args.seed))
+    lm_head = None
+    if args.sweep == "datasets":
+        g = torch.Generator(device="cuda").manual_seed(args.seed + 2)
+        lm_head = (torch.randn((shape.vocab, shape.d_model), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    torch.cuda.synchronize()
+    log(f"sweep {args.sweep}: model {args.model} ({shape.n_layers} layers), weights drawn on the device in "
+        f"{time.perf_counter() - t:.1f} s")
+    gen = torch.Generator(device="cuda").manual_seed(args.seed + 1)
+    out = {"sweep": args.sweep, "model": args.model, "shape": shape.__dict__, "seed": args.seed, "reps": args.reps,
+           "warmup": args.sweep_warmup}
+    if args.sweep == "dataset-packing":
+        out["pools"] = []
+        run_dataset_packing(pp, W, model, args, gen, out)
+        print(json.dumps(out), flush=True)
+        return
+    pools = args.pools.split(",") if args.sweep == "datasets" else [args.pool]
+    sizes = [int(b) for b in args.batch_sizes.split(",")] if args.sweep == "batch" else [args.batch]
+    out["per_batch_size"] = []
+    t0 = time.perf_counter()
+    for name in pools:
+        pool = sweep_pool(W, name, args.seed, args.prompts)
+        for bs in sizes:
+            n_b = len(pool) // bs
+            if args.max_batches:
+                n_b = min(n_b, args.max_batches)
+            recs = []
+            for b in range(n_b):
+                recs.append(measure_batch(pp, model, pool[b * bs:(b + 1) * bs], args, gen, lm_head))
+                if (b + 1) % 20 == 0 or b + 1 == n_b:
+                    log(f"  {name} batch size {bs}: {b + 1}/{n_b} batches, last speedup {recs[-1]['speedup']:.2f}x "
+                        f"({time.perf_counter() - t0:.0f} s)")
+                torch.cuda.empty_cache()
+            col = lambda key: np.array([r[key] for r in recs], dtype=np.float64)
+            sp, mp, md = col("speedup"), col("ms_packed"), col("ms_padded")
+            entry = {"pool": name, "prompts": int(len(pool)), "batch_size": bs, "batches": n_b,
+                     "speedup_mean": float(sp.mean()), "speedup_std": float(sp.std()),
+                     "ms_packed_mean": float(mp.mean()), "ms_packed_std": float(mp.std()),
+                     "ms_padded_mean": float(md.mean()), "ms_padded_std": float(md.std()),
+                     "total_time_ratio": float(md.sum() / mp.sum()),
+                     "r_over_k_mean": float(col("r_over_k").mean()), "max_abs_dev_mean": float(col("max_abs_dev").mean()),
+                     "tflops_packed_mean": float(col("tflops_packed").mean())}
+            if lm_head is not None:
+                tp, td = col("ttft_ms_packed"), col("ttft_ms_padded")
+                entry.update({"ttft_ms_packed_mean": float(tp.mean()), "ttft_ms_packed_std": float(tp.std()),
+                              "ttft_ms_padded_mean": float(td.mean()), "ttft_ms_padded_std": float(td.std()),
+                              "ttft_speedup_mean": float(col("ttft_speedup").mean())})
+            if n_b >= 3:
+                entry["fit_r_over_k"] = linear_fit(col("r_over_k"), sp)
+                entry["fit_max_abs_dev"] = linear_fit(col("max_abs_dev"), sp)
+            if args.sweep == "regression":
+                entry["records"] = recs
+            out["per_batch_size"].append(entry)
+            log(f"{name} batch size {bs}: speedup {entry['speedup_mean']:.2f} +- {entry['speedup_std']:.2f}x over "
+                f"{n_b} batches; packed {entry['ms_packed_mean']:.2f} ms, padded {entry['ms_padded_mean']:.2f} ms")
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -175,6 +398,23 @@ def main():
                     help="run only the dominant kernel and the calibration copy (for counter passes)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with the calibration copy (for byte-counter passes over the whole step)")
+    ap.add_argument("--sweep", choices=["regression", "batch", "datasets", "dataset-packing"],
+                    help="instead of the benchmark line: packing against full batching per batch of a prompt "
+                         "pool, with linear fits of the speedup (regression), across batch sizes (batch), with "
+                         "the time to first token over dataset stand-ins (datasets), or against length-ordered "
+                         "batching and whole-set packing (dataset-packing)")
+    ap.add_argument("--pool", default="uniform", help="sweep regression/batch: uniform (U[1,512]) or a dataset "
+                                                     "stand-in (wiki256, wiki512, mmlu, hh-rlhf, alpaca, samsum)")
+    ap.add_argument("--pools", default="wiki256,wiki512,mmlu,hh-rlhf,alpaca,samsum",
+                    help="sweep datasets/dataset-packing: prompt pools")
+    ap.add_argument("--model", default="llama-1.3b", help="sweep model shape (llama-1.3b, llama2-7b, mistral-7b)")
+    ap.add_argument("--layers", type=int, default=0, help="sweep: decoder layers (0 = the model's full depth)")
+    ap.add_argument("--batch", type=int, default=32, help="sweep: prompts (dataset packing: rows) per batch")
+    ap.add_argument("--batch-sizes", default="1,2,4,8,16,32,64", help="sweep batch: batch sizes")
+    ap.add_argument("--prompts", type=int, default=5000, help="sweep: prompts taken from the pool")
+    ap.add_argument("--max-batches", type=int, default=0, help="sweep: at most this many batches per size")
+    ap.add_argument("--reps", type=int, default=3, help="sweep: timed steps per batch and layout (median)")
+    ap.add_argument("--sweep-warmup", type=int, default=1, help="sweep: untimed steps per batch and layout")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -193,6 +433,9 @@ def main():
     torch.cuda.set_device(0)
     if args.traffic_pass:
         traffic_pass(args)
+        return
+    if args.sweep:
+        run_sweep(args)
         return
 
     t = time.perf_counter()

@@ -234,13 +234,15 @@ class DeviceModel:
         self.torch_dtype = dt
 
         def dev(a, t=dt):
+            if isinstance(a, torch.Tensor):          # already drawn with torch (device or host)
+                return a.to(device=device, dtype=t)
             return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device=device).to(t)
 
         self.embed = dev(weights["embed"])
         self.final_norm = dev(weights["final_norm"], torch.float32)
         self.layers: List[Dict] = []
         for L in weights["layers"][: shape.n_layers]:
-            wqkv = dev(np.concatenate([L["wq"], L["wk"], L["wv"]], axis=0))
+            wqkv = torch.cat([dev(L["wq"]), dev(L["wk"]), dev(L["wv"])], dim=0)
             self.layers.append(dict(
                 attn_norm=dev(L["attn_norm"], torch.float32), wqkv=wqkv, wo=dev(L["wo"]),
                 mlp_norm=dev(L["mlp_norm"], torch.float32),

@@ -28,9 +28,10 @@ from dataclasses import dataclass, field
 from typing import Callable, Dict, List, Optional
 
 import numpy as np
+from statistics import NormalDist
 
 __all__ = [
-    "ModelShape", "Workload", "Case", "WORKLOADS", "workload", "make_case",
+    "ModelShape", "Workload", "Case", "WORKLOADS", "MODELS", "DATASETS", "workload", "make_case",
     "draw_lengths", "draw_tokens", "draw_weights", "bf16_bits", "bf16_value",
 ]
 
@@ -121,6 +122,61 @@ WORKLOADS: Dict[int, Workload] = {
                 k=48, capacity=32768, lengths=_zipf(1.5, 32, 32768),
                 description="1.3B shape, 24 layers, bf16; 48 prompts 32*Zipf(1.5) clipped to "
                             "32768; rows of 32768"),
+}
+
+
+# Prompt pools for the batch-size and regression sweeps (the paper's section on how the gain
+# scales with the lengths in a batch, and its batch-size ablation): 5000 synthetic prompts with
+# lengths uniform in [1, 512], taken in draw order in batches of k, each batch packed with the
+# bin size equal to its own maximum length (capacity 0).  The model is chosen separately from
+# MODELS; ``k`` here is the pool size, not a batch size.
+WORKLOADS[6] = Workload(6, "uniform-1-512-pool", _LLAMA2_7B.replace(n_layers=24, d_model=2048, n_heads=16,
+                                                                   n_kv_heads=16, ffn_dim=5504),
+                        k=5000, capacity=0, lengths=_uniform(1, 512),
+                        description="5000 prompts U[1,512] in draw order, batched k at a time, "
+                                    "bin size = batch maximum")
+
+
+def _lognormal_from_stats(lo: int, mean: float, hi: int, n: int):
+    """Stand-in for a dataset known only by the min / mean / max of an n-prompt subsample:
+    a lognormal whose mean is the stated mean and whose (1 - 1/n) quantile, where the largest
+    of n draws sits, is the stated maximum; rounded and clipped to [min, max]."""
+    z = NormalDist().inv_cdf(1.0 - 1.0 / n)
+    c = float(np.log(hi / mean))            # = z sigma - sigma^2 / 2
+    sigma = z - float(np.sqrt(z * z - 2.0 * c))
+    mu = float(np.log(mean)) - sigma * sigma / 2.0
+
+    def f(rng: np.random.Generator, k: int) -> np.ndarray:
+        return np.clip(np.rint(rng.lognormal(mu, sigma, k)), lo, hi)
+    return f
+
+
+# Stand-ins for the paper's evaluation datasets (appendix table of dataset length statistics:
+# 1000-prompt subsamples, min / mean / max prompt length).  The texts are not available, and
+# only the lengths matter to the prefill cost.
+DATASETS = {
+    # name: (workload id, min, mean, max)
+    "wiki256": (7, 1, 73, 256),
+    "wiki512": (8, 6, 120, 512),
+    "mmlu": (9, 4, 64, 1102),
+    "hh-rlhf": (10, 22, 247, 1620),
+    "alpaca": (11, 43, 126, 527),
+    "samsum": (12, 21, 169, 942),
+}
+for _name, (_wid, _lo, _mean, _hi) in DATASETS.items():
+    WORKLOADS[_wid] = Workload(_wid, f"{_name}-standin", WORKLOADS[6].shape, k=1000, capacity=0,
+                               lengths=_lognormal_from_stats(_lo, _mean, _hi, 1000),
+                               description=f"1000 prompts standing in for {_name} (min {_lo}, mean {_mean}, "
+                                           f"max {_hi}): lognormal matched to the mean and to the max as the "
+                                           f"0.999 quantile, clipped")
+
+# Full-depth model shapes of the paper's appendix model table (bf16, random-init); Mistral 7B
+# adds grouped-query attention (8 key/value heads) and a 14336-wide FFN.  Its sliding window
+# (4096) is wider than every prompt of the sweeps, so plain causal attention is exact there.
+MODELS: Dict[str, ModelShape] = {
+    "llama-1.3b": _LLAMA2_7B.replace(n_layers=24, d_model=2048, n_heads=16, n_kv_heads=16, ffn_dim=5504),
+    "llama2-7b": _LLAMA2_7B.replace(n_layers=32),
+    "mistral-7b": _LLAMA2_7B.replace(n_layers=32, n_kv_heads=8, ffn_dim=14336),
 }
 
 
