@@ -162,7 +162,7 @@ def cpu_baseline(case, budget_s):
 
 # ----------------------------------------------------------------------------- sweeps
 def batch_predictors(lengths, n_rows):
-    """The two batch statistics the paper regresses the speedup on (section 4.6): the batch-size
+    """The two batch statistics the paper regresses the speedup on (section 4.7): the batch-size
     reduction r/k (packed rows over prompts) and the max absolute deviation m - L/k (the longest
     prompt minus the mean length)."""
     import numpy as np
@@ -247,7 +247,7 @@ def sweep_pool(W, name, seed, n):
 
 
 def dataset_batches(pp, lengths, bs):
-    """The four ways of batching a whole prompt set that the paper compares (section 4.5), as
+    """The four ways of batching a whole prompt set that the paper compares (section 4.6), as
     lists of (prompt ids, plan):
       full       batches of bs prompts in arrival (draw) order, right-padded to the batch maximum;
       batch      the same batches, each packed on its own (FFD, bin size = the batch maximum);
@@ -283,7 +283,7 @@ def dataset_batches(pp, lengths, bs):
 
 
 def run_dataset_packing(pp, W, model, args, gen, out):
-    """Per-prompt prefill time of the four batchings of each prompt set (section 4.5)."""
+    """Per-prompt prefill time of the four batchings of each prompt set (section 4.6)."""
     import numpy as np
     import torch
     shape = model.shape

@@ -17,7 +17,11 @@ defines, in float64 unless a caller asks for another precision:
                          appendix model table), in three modes that the paper
                          claims agree exactly (section 3.3): every prompt
                          alone, packed rows under the literal independent mask
-                         M' (section 3.2), and right-padded full batching.
+                         M' (section 3.2), and right-padded full batching;
+                         and the greedy first token of every prompt;
+* ``oracle.generate`` -- greedy generation after the prefill (sections 2.2
+                         and 4.8) by full recomputation for every token, and
+                         the teacher-forced rows a decode step must produce.
 
 It shares no code with the HIP path; the only thing both sides share are the
 seeded input generators in ``paper_2404_09529_amd.workloads``, which hold no

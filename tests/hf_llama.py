@@ -72,3 +72,30 @@ def additive_mask(allowed):
     m = torch.zeros(allowed.shape, dtype=torch.float64)
     m[~torch.from_numpy(allowed)] = torch.finfo(torch.float64).min
     return m[:, None]
+
+
+def greedy_generate(shape, weights, lm_head, ids, n_tokens):
+    """Hugging Face's greedy generate (its own incremental decoding with a KV cache) on one
+    prompt: the n_tokens new ids, and per layer the cached K, V of the positions after the
+    prompt ([n_tokens - 1, Hkv*D]: the last token is chosen but never fed)."""
+    from transformers import GenerationConfig, LlamaForCausalLM
+    base = build(shape, weights)
+    lm = LlamaForCausalLM(base.config).double().eval()
+    lm.model = base
+    lm.lm_head.weight.data = torch.from_numpy(np.asarray(lm_head, dtype=np.float64))
+    gc = GenerationConfig(max_new_tokens=n_tokens, min_new_tokens=n_tokens, do_sample=False, num_beams=1,
+                          eos_token_id=None, pad_token_id=0, bos_token_id=None)
+    gc.return_dict_in_generate, gc.use_cache = True, True
+    ids_t = torch.as_tensor(ids, dtype=torch.long)[None]
+    with torch.no_grad():   # an explicit mask: otherwise ids equal to the pad id would be masked out
+        out = lm.generate(input_ids=ids_t, attention_mask=torch.ones_like(ids_t), generation_config=gc)
+    l = len(ids)
+    new = out.sequences[0, l:].numpy()
+    ks, vs = [], []
+    for layer in out.past_key_values.layers:
+        k = layer.keys.numpy()[0]        # [Hkv, n, D]
+        v = layer.values.numpy()[0]
+        hk, n, d = k.shape
+        ks.append(k.transpose(1, 0, 2).reshape(n, hk * d)[l:])
+        vs.append(v.transpose(1, 0, 2).reshape(n, hk * d)[l:])
+    return new, ks, vs

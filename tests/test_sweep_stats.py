@@ -1,4 +1,4 @@
-"""Host-side statistics of the batch-size and regression sweeps (section 4.6 of the paper):
+"""Host-side statistics of the batch-size and regression sweeps (section 4.7 of the paper):
 the two predictors of the speedup, batch-size reduction r/k and max absolute deviation
 m - L/k, and the least-squares line fitted to them.  CPU only, no GPU work."""
 import os
