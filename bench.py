@@ -308,6 +308,88 @@ def run_dataset_packing(pp, W, model, args, gen, out):
         out["pools"].append(entry)
 
 
+def decode_step_bytes(shape, lengths, n_new, padded):
+    """Algorithmic HBM bytes of the n_new decode steps of one generate call: every step reads
+    all decoder weights, the LM head and the keys and values of every prompt's cache so far
+    (full batching: its padding too), and writes one key and value row per prompt."""
+    import numpy as np
+    s = shape
+    e = 2 if s.dtype == "bf16" else 4
+    d, H, Hkv, D, F, V = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim, s.ffn_dim, s.vocab
+    weights = s.n_layers * (d * (H + 2 * Hkv) * D + H * D * d + 3 * d * F) * e + V * d * e
+    lengths = np.asarray(lengths, dtype=np.int64)
+    ctx = len(lengths) * int(lengths.max()) if padded else int(lengths.sum())
+    k = len(lengths)
+    kv_row = 2 * s.n_layers * Hkv * D * e                    # one token's key and value, all layers
+    total = 0
+    for t in range(n_new):
+        total += weights + (ctx + k * (t + 1)) * kv_row      # reads (the step's own row included) ...
+        total += k * kv_row                                  # ... and the appended rows
+    return total
+
+
+def run_generate(args):
+    """Greedy generation after the prefill with packed and with full-batching KV caches
+    (section 4.8): --gen-lengths prompts (default: the paper's toy batch, nine prompts of one
+    token and one of 1000), --gen-tokens decode steps after the first token, on --model.
+    Times whole pp_generate calls (prefill and first token excluded), and reports the KV cache
+    and peak device memory of each layout."""
+    import numpy as np
+    import torch
+
+    from paper_2404_09529_amd import prepack as pp
+    from paper_2404_09529_amd import workloads as W
+
+    shape = W.MODELS[args.model]
+    if args.layers:
+        shape = shape.replace(n_layers=args.layers)
+    lengths = np.asarray([int(x) for x in args.gen_lengths.split(",")], dtype=np.int32)
+    n_new = args.gen_tokens
+    model = pp.DeviceModel(shape, device_weights(shape, args.seed))
+    g = torch.Generator(device="cuda").manual_seed(args.seed + 2)
+    lm = (torch.randn((shape.vocab, shape.d_model), generator=g, device="cuda") * 0.02).to(model.torch_dtype)
+    tokens = torch.randint(0, shape.vocab, (int(lengths.sum()),), generator=g, device="cuda", dtype=torch.int32)
+    dplan = pp.DevicePlan(pp.pp_pack(lengths, 0))
+    pre = pp.Prefill(model, dplan)
+    pre(tokens)
+    ws = torch.empty(max(pp.pp_first_token_workspace_size(model.config, dplan), 1), dtype=torch.uint8, device="cuda")
+    first = torch.empty(len(lengths), dtype=torch.int32, device="cuda")
+    pp.pp_first_token(model.config, dplan, pre.hidden, lm, ws, first)
+    torch.cuda.synchronize()
+    base_alloc = torch.cuda.memory_allocated()
+    out = {"generate": args.model, "shape": shape.__dict__, "lengths": lengths.tolist(), "n_new": n_new,
+           "reps": args.reps, "warmup": args.sweep_warmup}
+    toks = {}
+    for name, padded in (("packed", False), ("padded", True)):
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        gen = pp.Generation(model, pre, lengths, n_new, padded=padded)
+        stream = torch.cuda.current_stream()
+        t = time_steps(lambda: gen(first, lm, stream=stream), args.reps, args.sweep_warmup)
+        torch.cuda.synchronize()
+        toks[name] = gen.tokens.cpu().numpy()
+        nbytes = decode_step_bytes(shape, lengths, n_new, padded)
+        ms = t["ms_median"]
+        out[name] = {"ms": ms, "ms_per_token": ms / n_new, "ms_p10": t["ms_p10"], "ms_p90": t["ms_p90"],
+                     "kv_cache_bytes": gen.kv_cache_bytes(),
+                     "peak_alloc_bytes": int(torch.cuda.max_memory_allocated()),
+                     "extra_alloc_bytes": int(torch.cuda.max_memory_allocated() - base_alloc),
+                     "algorithmic_bytes": nbytes,
+                     "roofline": {"bound": "hbm", "achieved": round(nbytes / (ms / 1e3) / 1e9, 1),
+                                  "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                                  "frac": round(nbytes / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS, 4)}}
+        log(f"{name}: {ms:.3f} ms for {n_new} tokens ({ms / n_new:.3f} ms/token), KV cache "
+            f"{gen.kv_cache_bytes() / 1e6:.1f} MB, peak {torch.cuda.max_memory_allocated() / 1e9:.2f} GB, "
+            f"{nbytes / (ms / 1e3) / 1e9:.0f} GB/s algorithmic")
+        del gen
+        torch.cuda.empty_cache()
+    out["tokens_identical"] = bool(np.array_equal(toks["packed"], toks["padded"]))
+    out["time_saving"] = 1.0 - out["packed"]["ms"] / out["padded"]["ms"]
+    out["kv_memory_saving"] = 1.0 - out["packed"]["kv_cache_bytes"] / out["padded"]["kv_cache_bytes"]
+    out["peak_memory_saving"] = 1.0 - out["packed"]["peak_alloc_bytes"] / out["padded"]["peak_alloc_bytes"]
+    print(json.dumps(out), flush=True)
+
+
 def run_sweep(args):
     """--sweep regression: batches of --batch prompts from the prompt pool, the speedup of
     packing over full batching per batch, and the linear fits of the speedup on r/k and on
@@ -415,6 +497,11 @@ def main():
     ap.add_argument("--max-batches", type=int, default=0, help="sweep: at most this many batches per size")
     ap.add_argument("--reps", type=int, default=3, help="sweep: timed steps per batch and layout (median)")
     ap.add_argument("--sweep-warmup", type=int, default=1, help="sweep: untimed steps per batch and layout")
+    ap.add_argument("--generate", action="store_true",
+                    help="instead of the benchmark line: greedy generation with packed vs full-batching KV caches")
+    ap.add_argument("--gen-lengths", default=",".join(["1"] * 9 + ["1000"]),
+                    help="generate: prompt lengths (default: nine of one token and one of 1000)")
+    ap.add_argument("--gen-tokens", type=int, default=20, help="generate: decode steps after the first token")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -436,6 +523,9 @@ def main():
         return
     if args.sweep:
         run_sweep(args)
+        return
+    if args.generate:
+        run_generate(args)
         return
 
     t = time.perf_counter()

@@ -307,6 +307,93 @@ pp_status pp_first_token_workspace_size(const pp_config* cfg, const pp_dplan* pl
 pp_status pp_first_token(const pp_config* cfg, const pp_dplan* plan, const float* hidden, const void* lm_head,
                          void* workspace, size_t workspace_bytes, float* logits, int32_t* tokens, void* stream);
 
+/* ------------------------------------------------------------------------------------------
+ * Generation with packed KV caches (section 4.8: the caches of a batch are packed for
+ * generation instead of padded to the longest prompt; section 2.2: one forward pass per new
+ * token, the keys and values of earlier tokens read from the cache).  Greedy decoding: each
+ * step feeds one token per prompt and chooses the next as pp_first_token does.
+ * ---------------------------------------------------------------------------------------- */
+
+/* Where the keys and values of each prompt live during generation.  At decode step s
+ * (0 <= s < n_new) prompt i's keys are, in this order, the ctx_span[i] rows of the context
+ * cache from row ctx_off[i] (the first ctx_valid[i] of them its prompt tokens, the rest
+ * full batching's padding, read and masked), then rows gen_off[i] .. gen_off[i] + s of the
+ * generation cache, the last of which step s writes.  The token fed at step s sits at
+ * position pos0[i] + s (each prompt's own positions continue; section 3.2).
+ *
+ *   packed (padded == 0): the context cache is pp_prefill's per-prompt cache (ctx_off[i] =
+ *          l_0 + .. + l_{i-1}, ctx_span = ctx_valid = l_i, ctx_rows = total length); the
+ *          generation cache holds n_new rows per prompt (gen_off[i] = i n_new,
+ *          gen_rows = k n_new).  Nothing is padded.
+ *   padded (padded == 1): full batching: one cache of k rows of m + n_new slots (m = the
+ *          longest prompt), prompt i at row i (m + n_new), its padding up to m read and
+ *          masked, its generated tokens from slot m on (ctx_span = m, ctx_valid = l_i,
+ *          gen_off[i] = i (m + n_new) + m, ctx_rows = gen_rows = k (m + n_new)): context and
+ *          generation cache are then the same buffer.
+ * pos0[i] = l_i in both.  max_len = m.  The five arrays are [k] int32, caller-owned. */
+typedef struct pp_gen_layout {
+    int32_t k, n_new, padded, max_len;
+    int64_t ctx_rows, gen_rows;        /* rows per layer of the context / generation caches */
+    int32_t *ctx_off, *ctx_span, *ctx_valid, *pos0, *gen_off;
+} pp_gen_layout;
+
+/* The same layout with its five arrays in device memory: what the decode calls read. */
+typedef struct pp_gen_dlayout {
+    int32_t k, n_new, padded, max_len;
+    int64_t ctx_rows, gen_rows;
+    const int32_t *ctx_off, *ctx_span, *ctx_valid, *pos0, *gen_off;
+} pp_gen_dlayout;
+
+/* Fill `layout` (its arrays allocated by the caller, [k] each) for prompts of the given
+ * lengths, room for n_new generated tokens each, packed (padded == 0) or full batching.
+ * Pure host code, reentrant.
+ * Errors: PP_ERR_INVALID_ARG (k <= 0, a length <= 0, n_new <= 0, padded not 0/1, NULL array,
+ *         more than 2^31 - 1 rows). */
+pp_status pp_gen_layout_make(const int32_t* lengths, int32_t k, int32_t n_new, int32_t padded,
+                             pp_gen_layout* layout);
+
+/* Bytes of device workspace pp_decode_step and pp_generate need for this config and layout.
+ * Errors: as pp_decode_step's argument checks. */
+pp_status pp_decode_workspace_size(const pp_config* cfg, const pp_gen_dlayout* layout, size_t* bytes);
+
+/* Decode step `step` for every prompt: embed tokens_in[i] (the token chosen before: the
+ * first token of pp_first_token at step 0), run the decoder on that one row per prompt at
+ * position pos0[i] + step (RoPE, attention over the prompt's own keys only, MLP), append its
+ * key and value to the generation cache at row gen_off[i] + step of every layer, apply the
+ * final norm and the LM head, and choose tokens_out[i] greedily (as pp_first_token: the
+ * lowest id of maximal logit, -1 if every logit is NaN).
+ *
+ *   tokens_in, tokens_out  device int32 [k]
+ *   lm_head   device [vocab, d] in the config dtype
+ *   ctx_k, ctx_v  device [n_layers][ctx_rows][Hkv D] in dtype: read only
+ *   gen_k, gen_v  device [n_layers][gen_rows][Hkv D] in dtype: rows gen_off[i] + step are
+ *             written, earlier generated rows read (in the padded layout the same buffers
+ *             as ctx_k, ctx_v)
+ *   workspace device, >= pp_decode_workspace_size bytes, 256-byte aligned
+ *   logits    device float32 [k, vocab], or NULL
+ *   stream    a hipStream_t (NULL = the default stream)
+ *
+ * Numerics as pp_prefill (bf16 storage of weights, activations, q/k/v and caches; float32
+ * accumulation, softmax and residual stream), and as pp_first_token for the choice.  The
+ * packed and the full-batching layouts give bit-identical results.  Asynchronous; validated
+ * before enqueuing; the layout's device arrays are trusted to be what pp_gen_layout_make
+ * wrote.
+ * Errors: PP_ERR_INVALID_ARG (NULL pointer, step outside [0, n_new), inconsistent layout,
+ *         misaligned workspace), PP_ERR_BUFFER_TOO_SMALL (workspace), PP_ERR_UNSUPPORTED
+ *         (as pp_prefill, and H / Hkv not in {1, 2, 4, 8}), PP_ERR_HIP (launch failure). */
+pp_status pp_decode_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayout* layout, int32_t step,
+                         const int32_t* tokens_in, const void* lm_head, const void* ctx_k, const void* ctx_v,
+                         void* gen_k, void* gen_v, void* workspace, size_t workspace_bytes, float* logits,
+                         int32_t* tokens_out, void* stream);
+
+/* n_steps <= n_new decode steps back to back on `stream`, with no host synchronisation:
+ * step s consumes tokens[s - 1] (tokens_first at s = 0) and writes tokens[s]; tokens is
+ * device int32 [n_steps][k].  Same buffers and errors as pp_decode_step. */
+pp_status pp_generate(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayout* layout, int32_t n_steps,
+                      const int32_t* tokens_first, const void* lm_head, const void* ctx_k, const void* ctx_v,
+                      void* gen_k, void* gen_v, void* workspace, size_t workspace_bytes, int32_t* tokens,
+                      void* stream);
+
 #ifdef __cplusplus
 }
 #endif

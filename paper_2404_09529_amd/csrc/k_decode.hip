@@ -1,0 +1,455 @@
+// Generation with packed KV caches (section 4.8): the kernels of one decode step that the
+// prefill does not already have.  Each step feeds one new token per prompt through the
+// decoder (section 2.2: one forward pass per token, earlier keys and values read from the
+// cache); the projections reuse the prefill's GEMMs with one row per prompt.
+//
+// decode_prep_kernel     per prompt: the token's position pos0 + step (restart positions,
+//                        section 3.2, continued into generation), cos/sin of that position
+//                        for RoPE (evaluated in float64 as in the prefill's table), the
+//                        generation-cache row the step appends to, and identity indices.
+// decode_attn_kernel     split-key attention of one query row per prompt against that
+//                        prompt's keys only: context rows (its prompt tokens, plus masked
+//                        padding in the full-batching layout) and the generated rows so far.
+//                        A workgroup takes one (prompt, key/value head, chunk of 256 keys)
+//                        and all query heads of the group, so every key and value is read
+//                        from HBM once per step; it writes the chunk's (max, sum, output).
+// decode_combine_kernel  merges a prompt's chunk results in a fixed order.
+// skinny_gemm_kernel     the projections of a decode step, one row per prompt (k <= 64):
+//                        C[k, N] = A[k, K] W[N, K]^T is bound by streaming W from HBM, so
+//                        the work is cut into 64-row x K-split pieces that occupy every CU:
+//                        each workgroup stages its slice of A (all k rows) in LDS once, and
+//                        each of its 4 wavefronts streams 16 rows of W straight from HBM into
+//                        registers, all its K steps requested up front, into the 16x16x32
+//                        bf16 MFMA (W rows x prompts).  Float32 partial sums per K split.
+// decode_epilogue_kernel sums the K splits in a fixed order and applies the epilogue: the
+//                        residual add, SwiGLU over the interleaved gate/up rows, or RoPE at
+//                        the token's position with the query store and the key/value append.
+//
+// The chunks of the context part are counted from the prompt's first key, and the
+// generated keys form chunks of their own, so the packed and the full-batching layouts give
+// each valid key the same chunk and lane: their results are bit-identical, the padding
+// contributing exact zeros.
+#include <math.h>
+
+#include <algorithm>
+
+#include "device.h"
+#include "kernels.h"
+#include "prepack.h"
+
+namespace {
+
+constexpr int CH = ppk::kDecodeChunk;   // keys per chunk: 4 wavefronts x 8 iterations x 8 keys
+constexpr float kLog2e = 1.4426950408889634f;
+
+__global__ __launch_bounds__(64) void decode_prep_kernel(int k, int step, const int32_t* __restrict__ pos0,
+                                                         const int32_t* __restrict__ gen_off, int D, double theta,
+                                                         float2* __restrict__ table, int32_t* __restrict__ slot_pos,
+                                                         int32_t* __restrict__ slot_kv, int32_t* __restrict__ slot_seg,
+                                                         int32_t* __restrict__ ident) {
+    const int i = blockIdx.x, j = threadIdx.x;
+    if (i >= k) return;
+    const int half = D / 2;
+    if (j < half) {
+        const double inv_freq = pow(theta, -2.0 * j / static_cast<double>(D));
+        const double a = static_cast<double>(pos0[i] + step) * inv_freq;
+        table[int64_t(i) * half + j] = make_float2(static_cast<float>(cos(a)), static_cast<float>(sin(a)));
+    }
+    if (j == 0) {
+        slot_pos[i] = i;                 // row i of this step's table
+        slot_kv[i] = gen_off[i] + step;  // the row this step appends to
+        slot_seg[i] = 0;
+        ident[i] = i;
+        if (i == k - 1) ident[k] = k;
+    }
+}
+
+template <typename T, int DL>
+__device__ __forceinline__ void load_slice(const T* p, float* v) {
+#pragma unroll
+    for (int e = 0; e < DL; e += 8) load8(p + e, v + e);
+}
+
+// (m, l, o) <- merge of two partial softmax results over disjoint key sets (base-2 scores).
+template <int DL>
+__device__ __forceinline__ void merge(float& m, float& l, float* o, float m2, float l2, const float* o2) {
+    const float M = fmaxf(m, m2);
+    const float a = M == -INFINITY ? 0.f : exp2f(m - M);
+    const float b = M == -INFINITY ? 0.f : exp2f(m2 - M);
+    l = l * a + l2 * b;
+#pragma unroll
+    for (int e = 0; e < DL; ++e) o[e] = o[e] * a + o2[e] * b;
+    m = M;
+}
+
+// Lane l of wavefront w: key group kg = l / 8 (one key per iteration), dimension slice
+// dl = l % 8 (D / 8 consecutive elements).  Keys of the chunk: j0 + 64 w + 8 it + kg.
+template <typename T, int D, int R>
+__global__ __launch_bounds__(256) void decode_attn_kernel(
+    const T* __restrict__ q, int64_t ldq, const T* __restrict__ ctx_k, const T* __restrict__ ctx_v,
+    const T* __restrict__ gen_k, const T* __restrict__ gen_v, int64_t ldkv, const int32_t* __restrict__ ctx_off,
+    const int32_t* __restrict__ ctx_span, const int32_t* __restrict__ ctx_valid, const int32_t* __restrict__ gen_off,
+    int step, int Hkv, int n_ctx_chunks, int n_chunks, float* __restrict__ part) {
+    constexpr int DL = D / 8;
+    constexpr int PS = D + 4;            // floats per partial: o[D], m, l, 2 unused
+    __shared__ float red[4][R][D + 2];
+    const int i = blockIdx.x / Hkv, g = blockIdx.x % Hkv, c = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int kg = lane >> 3, dl = lane & 7;
+
+    const T* K;
+    const T* V;
+    int64_t row0;
+    int j0, jend, valid;
+    if (c < n_ctx_chunks) {
+        j0 = c * CH;
+        jend = min(j0 + CH, ctx_span[i]);
+        valid = ctx_valid[i];
+        row0 = ctx_off[i];
+        K = ctx_k;
+        V = ctx_v;
+    } else {
+        j0 = (c - n_ctx_chunks) * CH;
+        jend = min(j0 + CH, step + 1);
+        valid = step + 1;
+        row0 = gen_off[i];
+        K = gen_k;
+        V = gen_v;
+    }
+    if (j0 >= jend) return;              // past this prompt's keys: no partial, never combined
+
+    // queries of the group's R heads, pre-scaled so that scores are in base 2
+    const float scale = kLog2e * rsqrtf(static_cast<float>(D));
+    float qf[R][DL];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        load_slice<T, DL>(q + int64_t(i) * ldq + int64_t(g * R + r) * D + dl * DL, qf[r]);
+#pragma unroll
+        for (int e = 0; e < DL; ++e) qf[r][e] *= scale;
+    }
+    float m[R], l[R], o[R][DL];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        m[r] = -INFINITY;
+        l[r] = 0.f;
+#pragma unroll
+        for (int e = 0; e < DL; ++e) o[r][e] = 0.f;
+    }
+    const int64_t col = int64_t(g) * D + dl * DL;
+#pragma unroll 2
+    for (int it = 0; it < 8; ++it) {
+        const int j = j0 + 64 * w + 8 * it + kg;
+        const bool in = j < jend;
+        float kf[DL], vf[DL];
+        if (in) {
+            const int64_t off = (row0 + j) * ldkv + col;
+            load_slice<T, DL>(K + off, kf);
+            load_slice<T, DL>(V + off, vf);
+        } else {
+#pragma unroll
+            for (int e = 0; e < DL; ++e) kf[e] = vf[e] = 0.f;
+        }
+        const bool ok = in && j < valid;  // padding of the full-batching layout is read, then masked
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            float s = 0.f;
+#pragma unroll
+            for (int e = 0; e < DL; ++e) s = fmaf(qf[r][e], kf[e], s);
+            s += __shfl_xor(s, 1);
+            s += __shfl_xor(s, 2);
+            s += __shfl_xor(s, 4);
+            if (ok) {
+                const float mn = fmaxf(m[r], s);
+                const float a = exp2f(m[r] - mn);   // m = -inf at the first key: a = 0
+                const float p = exp2f(s - mn);
+                l[r] = l[r] * a + p;
+#pragma unroll
+                for (int e = 0; e < DL; ++e) o[r][e] = fmaf(p, vf[e], o[r][e] * a);
+                m[r] = mn;
+            }
+        }
+    }
+    // merge the 8 key groups of the wavefront (lanes with the same dl), then the 4 wavefronts
+#pragma unroll
+    for (int x = 8; x < 64; x <<= 1) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            float o2[DL];
+#pragma unroll
+            for (int e = 0; e < DL; ++e) o2[e] = __shfl_xor(o[r][e], x);
+            const float m2 = __shfl_xor(m[r], x), l2 = __shfl_xor(l[r], x);
+            merge<DL>(m[r], l[r], o[r], m2, l2, o2);
+        }
+    }
+    if (kg == 0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+#pragma unroll
+            for (int e = 0; e < DL; ++e) red[w][r][dl * DL + e] = o[r][e];
+            if (dl == 0) {
+                red[w][r][D] = m[r];
+                red[w][r][D + 1] = l[r];
+            }
+        }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < R * D; idx += 256) {
+        const int r = idx / D, e = idx % D;
+        float mm = red[0][r][D], ll = red[0][r][D + 1], oo = red[0][r][e];
+#pragma unroll
+        for (int w2 = 1; w2 < 4; ++w2) merge<1>(mm, ll, &oo, red[w2][r][D], red[w2][r][D + 1], &red[w2][r][e]);
+        float* pp = part + ((int64_t(i) * (Hkv * R) + g * R + r) * n_chunks + c) * PS;
+        pp[e] = oo;
+        if (e == 0) {
+            pp[D] = mm;
+            pp[D + 1] = ll;
+        }
+    }
+}
+
+// One wavefront per (prompt, query head): the prompt's context chunks, then its generated
+// chunks, merged in that order; out = o / l.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void decode_combine_kernel(const float* __restrict__ part, int k, int H,
+                                                             const int32_t* __restrict__ ctx_span, int step,
+                                                             int n_ctx_chunks, int n_chunks, T* __restrict__ out,
+                                                             int64_t ldo) {
+    constexpr int PS = D + 4;
+    constexpr int E = D / 64;            // dimensions per lane
+    const int pair = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (pair >= k * H) return;
+    const int i = pair / H, h = pair % H;
+    const float* base = part + int64_t(pair) * n_chunks * PS;
+    float m = -INFINITY, l = 0.f, o[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[e] = 0.f;
+    const int nc = (ctx_span[i] + CH - 1) / CH, ng = (step + 1 + CH - 1) / CH;
+    for (int t = 0; t < nc + ng; ++t) {
+        const float* pp = base + int64_t(t < nc ? t : n_ctx_chunks + t - nc) * PS;
+        float o2[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) o2[e] = pp[lane * E + e];
+        merge<E>(m, l, o, pp[D], pp[D + 1], o2);
+    }
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    T* dst = out + int64_t(i) * ldo + int64_t(h) * D + lane * E;
+#pragma unroll
+    for (int e = 0; e < E; ++e) dst[e] = static_cast<T>(o[e] * inv);
+}
+
+// LDS swizzle of a staged A tile (rows of 128 bf16 = 256 bytes): row r's 16-byte chunk q at
+// q ^ gsw(r % 8), gsw placing r's bits 0, 1, 2 at bits 0, 2, 3.  A fragment read takes rows
+// r..r+15 at chunk 4 s + l / 16; the lanes served together (i and i + 32) then hit 16
+// distinct bank groups.
+__device__ __forceinline__ int gsw(int r) { return (r & 1) | (((r >> 1) & 1) << 2) | (((r >> 2) & 1) << 3); }
+
+constexpr int SG_ROWS = 64;     // W rows per workgroup, 16 per wavefront
+constexpr int SG_TILE = 128;    // K columns per staged A tile
+constexpr int SG_MAX_TILES = 4; // A tiles per K split (64 KB of LDS at 64 prompts)
+
+// part[s][m][n] = sum over the K tiles of split s of A[m, :] . W[n, :], for m < k <= 64.
+// Wavefront w owns W rows n0 = 64 blockIdx.x + 16 w .. + 15; lane l reads 8 consecutive K
+// values of row n0 + l % 16 at offset 8 (l / 16) of each 32-wide step, and holds, per prompt
+// block mb, the sums of prompt 16 mb + l % 16 for rows n0 + 4 (l / 16) + 0..3.
+__global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
+                                                          const bf16* __restrict__ W, int64_t ldw, int N, int K,
+                                                          int tiles_per_split, float* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) char lds[SG_MAX_TILES][64 * 256];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lr = lane & 15, q4 = lane >> 4;
+    const int s = blockIdx.y;
+    const int t0 = s * tiles_per_split, nt = min(tiles_per_split, K / SG_TILE - t0);
+    const int nmb = (k + 15) / 16, k_pad = 16 * nmb;
+    // stage A[0 .. k_pad) x tiles t0 .. t0 + nt (rows past k read as row k - 1, never stored)
+    for (int idx = threadIdx.x; idx < k_pad * nt * 16; idx += 256) {
+        const int r = idx / (nt * 16), q = idx % (nt * 16), t = q / 16, ch = q % 16;
+        const bf16x8 v = *reinterpret_cast<const bf16x8*>(A + int64_t(min(r, k - 1)) * lda +
+                                                          int64_t(t0 + t) * SG_TILE + ch * 8);
+        *reinterpret_cast<bf16x8*>(lds[t] + r * 256 + 16 * (ch ^ gsw(r & 7))) = v;
+    }
+    const int n0 = blockIdx.x * SG_ROWS + 16 * w;
+    const bf16* wrow = W + int64_t(n0 + lr) * ldw + int64_t(t0) * SG_TILE + 8 * q4;
+    const int steps = 4 * nt;
+    bf16x8 ring[4 * SG_MAX_TILES];
+#pragma unroll
+    for (int j = 0; j < 4 * SG_MAX_TILES; ++j)
+        if (j < steps) ring[j] = *reinterpret_cast<const bf16x8*>(wrow + 32 * j);
+    __syncthreads();
+    f32x4 acc[4] = {};
+    const int fsw = gsw(lr & 7);
+#pragma unroll
+    for (int j = 0; j < 4 * SG_MAX_TILES; ++j) {
+        if (j >= steps) break;
+        const char* tile = lds[j / 4];
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) {
+            if (mb >= nmb) break;
+            const bf16x8 h = *reinterpret_cast<const bf16x8*>(tile + (16 * mb + lr) * 256 +
+                                                              16 * ((4 * (j % 4) + q4) ^ fsw));
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[j], h, acc[mb], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+        const int m = 16 * mb + lr;
+        if (mb < nmb && m < k)
+            *reinterpret_cast<f32x4*>(part + (int64_t(s) * k + m) * N + n0 + 4 * q4) = acc[mb];
+    }
+}
+
+// Sum of the K splits of part at (m, n .. n + 3), in split order.
+__device__ __forceinline__ f32x4 split_sum(const float* part, int S, int k, int N, int m, int n) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(part + int64_t(m) * N + n);
+    for (int s = 1; s < S; ++s) v += *reinterpret_cast<const f32x4*>(part + (int64_t(s) * k + m) * N + n);
+    return v;
+}
+
+// One thread per 4 consecutive outputs of one prompt row.
+template <int EPI>
+__global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __restrict__ part, int S, int k, int N,
+                                                              ppk::DecodeEpi ep) {
+    const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (EPI == ppk::kResidual) {           // x[m][n] += sum
+        const int per = N / 4;
+        if (idx >= int64_t(k) * per) return;
+        const int m = static_cast<int>(idx / per), n = static_cast<int>(idx % per) * 4;
+        f32x4* x = reinterpret_cast<f32x4*>(static_cast<float*>(ep.out) + int64_t(m) * ep.ldo + n);
+        *x = *x + split_sum(part, S, k, N, m, n);
+    } else if (EPI == ppk::kSwiGLU) {      // out[m][f] = SiLU(gate) * up, gate/up rows interleaved by 16
+        const int F = N / 2, per = F / 4;
+        if (idx >= int64_t(k) * per) return;
+        const int m = static_cast<int>(idx / per), f = static_cast<int>(idx % per) * 4;
+        const int g = 32 * (f / 16) + f % 16;
+        const f32x4 gt = split_sum(part, S, k, N, m, g), up = split_sum(part, S, k, N, m, g + 16);
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(gt[e]) * up[e]);
+        *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + f) = o;
+    } else {                               // QKV: RoPE on q and k (pairs i, i + 64), store / append
+        const ppk::QkvOut& qo = ep.qkv;
+        const int heads = qo.H + 2 * qo.Hkv, per = heads * 16;   // 16 quads per head of 128
+        if (idx >= int64_t(k) * per) return;
+        const int m = static_cast<int>(idx / per), r = static_cast<int>(idx % per);
+        const int head = r / 16, i = (r % 16) * 4;
+        const int n = head * 128 + i;
+        const f32x4 a = split_sum(part, S, k, N, m, n), b = split_sum(part, S, k, N, m, n + 64);
+        bf16x4 lo, hi;
+        if (head < qo.H + qo.Hkv) {
+            const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float2 t = cs[e];
+                lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
+                hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                lo[e] = static_cast<bf16>(a[e]);
+                hi[e] = static_cast<bf16>(b[e]);
+            }
+        }
+        bf16* dst;
+        if (head < qo.H) {
+            dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
+        } else {
+            const bool key = head < qo.H + qo.Hkv;
+            dst = static_cast<bf16*>(key ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
+                  (head - qo.H - (key ? 0 : qo.Hkv)) * 128;
+        }
+        *reinterpret_cast<bf16x4*>(dst + i) = lo;
+        *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+    }
+}
+
+template <typename T, int D, int R>
+void launch_attn(const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v, const void* gen_k,
+                 const void* gen_v, int64_t ldkv, const ppk::DecodeLayout& Ly, int step, int Hkv, float* part,
+                 hipStream_t s) {
+    const dim3 grid(Ly.k * Hkv, Ly.n_ctx_chunks + Ly.n_gen_chunks);
+    decode_attn_kernel<T, D, R><<<grid, 256, 0, s>>>(
+        static_cast<const T*>(q), ldq, static_cast<const T*>(ctx_k), static_cast<const T*>(ctx_v),
+        static_cast<const T*>(gen_k), static_cast<const T*>(gen_v), ldkv, Ly.ctx_off, Ly.ctx_span, Ly.ctx_valid,
+        Ly.gen_off, step, Hkv, Ly.n_ctx_chunks, Ly.n_ctx_chunks + Ly.n_gen_chunks, part);
+}
+
+template <typename T, int D>
+void attn_by_group(int R, const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v, const void* gen_k,
+                   const void* gen_v, int64_t ldkv, const ppk::DecodeLayout& Ly, int step, int Hkv, float* part,
+                   hipStream_t s) {
+    switch (R) {
+        case 1: launch_attn<T, D, 1>(q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, s); break;
+        case 2: launch_attn<T, D, 2>(q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, s); break;
+        case 4: launch_attn<T, D, 4>(q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, s); break;
+        default: launch_attn<T, D, 8>(q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, s); break;
+    }
+}
+
+template <typename T>
+void attn_dispatch(int D, int R, const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v,
+                   const void* gen_k, const void* gen_v, int64_t ldkv, const ppk::DecodeLayout& Ly, int step,
+                   int Hkv, float* part, void* out, int64_t ldo, hipStream_t s) {
+    const int H = Hkv * R;
+    const int blocks = (Ly.k * H + 3) / 4;
+    const int nch = Ly.n_ctx_chunks + Ly.n_gen_chunks;
+    if (D == 128) {
+        attn_by_group<T, 128>(R, q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, s);
+        decode_combine_kernel<T, 128><<<blocks, 256, 0, s>>>(part, Ly.k, H, Ly.ctx_span, step, Ly.n_ctx_chunks, nch,
+                                                             static_cast<T*>(out), ldo);
+    } else {
+        attn_by_group<T, 64>(R, q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, s);
+        decode_combine_kernel<T, 64><<<blocks, 256, 0, s>>>(part, Ly.k, H, Ly.ctx_span, step, Ly.n_ctx_chunks, nch,
+                                                            static_cast<T*>(out), ldo);
+    }
+}
+
+}  // namespace
+
+namespace ppk {
+
+void decode_prep(const DecodeLayout& Ly, int step, int D, float theta, float2* table, int32_t* slot_pos,
+                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, hipStream_t s) {
+    decode_prep_kernel<<<Ly.k, 64, 0, s>>>(Ly.k, step, Ly.pos0, Ly.gen_off, D, static_cast<double>(theta), table,
+                                           slot_pos, slot_kv, slot_seg, ident);
+}
+
+void decode_attention(int dtype, const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v,
+                      const void* gen_k, const void* gen_v, int64_t ldkv, const DecodeLayout& Ly, int step, int H,
+                      int Hkv, int D, float* part, void* out, int64_t ldo, hipStream_t s) {
+    const int R = H / Hkv;
+    if (dtype == PP_BF16)
+        attn_dispatch<bf16>(D, R, q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, out, ldo, s);
+    else
+        attn_dispatch<float>(D, R, q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, out, ldo, s);
+}
+
+SkinnySplit skinny_split(int N, int K) {
+    const int tiles = K / SG_TILE, groups = N / SG_ROWS;
+    const int target = std::max(1, (512 + groups - 1) / groups);   // about 512 workgroups
+    const int per = std::min(SG_MAX_TILES, std::max(1, (tiles + target - 1) / target));
+    return SkinnySplit{per, (tiles + per - 1) / per};
+}
+
+bool skinny_ok(int k, int N, int K) { return k >= 1 && k <= 64 && N % SG_ROWS == 0 && K % SG_TILE == 0; }
+
+void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
+                 const DecodeEpi& ep, hipStream_t s) {
+    const SkinnySplit sp = skinny_split(N, K);
+    skinny_gemm_kernel<<<dim3(N / SG_ROWS, sp.splits), 256, 0, s>>>(static_cast<const bf16*>(A), lda, k,
+                                                                      static_cast<const bf16*>(W), ldw, N, K,
+                                                                      sp.tiles_per_split, part);
+    int64_t threads;
+    if (epi == kResidual) threads = int64_t(k) * (N / 4);
+    else if (epi == kSwiGLU) threads = int64_t(k) * (N / 8);
+    else threads = int64_t(k) * (N / 128) * 16;           // (H + 2 Hkv) heads x 16 pairs of quads
+    const int blocks = static_cast<int>((threads + 255) / 256);
+    if (epi == kResidual)
+        decode_epilogue_kernel<kResidual><<<blocks, 256, 0, s>>>(part, sp.splits, k, N, ep);
+    else if (epi == kSwiGLU)
+        decode_epilogue_kernel<kSwiGLU><<<blocks, 256, 0, s>>>(part, sp.splits, k, N, ep);
+    else
+        decode_epilogue_kernel<kQkvRope><<<blocks, 256, 0, s>>>(part, sp.splits, k, N, ep);
+}
+
+}  // namespace ppk

@@ -92,4 +92,51 @@ size_t first_token_workspace(int dtype, int k, int V, int d);
 void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, int k, const void* lm_head, int V,
                  int d, void* workspace, float* logits, int32_t* tokens, hipStream_t s);
 
+// ---------------------------------------------------------------------- generation (decode)
+constexpr int kDecodeChunk = 256;   // keys per workgroup of the decode attention
+
+// Device view of a generation layout (pp_gen_dlayout) with the chunk counts of its keys:
+// n_ctx_chunks = ceil(max_len / kDecodeChunk), n_gen_chunks = ceil(n_new / kDecodeChunk).
+struct DecodeLayout {
+    int k, n_ctx_chunks, n_gen_chunks;
+    const int32_t *ctx_off, *ctx_span, *ctx_valid, *pos0, *gen_off;
+};
+
+// Per prompt i < k for decode step `step`: table[i] = cos/sin((pos0[i] + step) theta^(-2j/D))
+// for j < D/2 (float64, float2 [k][D/2]); slot_pos[i] = i; slot_kv[i] = gen_off[i] + step;
+// slot_seg[i] = 0; ident[i] = i for i <= k (k + 1 entries).
+void decode_prep(const DecodeLayout& Ly, int step, int D, float theta, float2* table, int32_t* slot_pos,
+                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, hipStream_t s);
+
+// One query row per prompt (q [k, ldq], H heads of D) against the prompt's context rows
+// ctx_off[i] .. + ctx_span[i] of ctx_k / ctx_v (rows past ctx_valid[i] masked) and its
+// generated rows gen_off[i] .. + step of gen_k / gen_v; row stride ldkv; GQA head h reads
+// key/value head h / (H / Hkv).  out [k, ldo] = softmax(q k^T / sqrt(D)) v, dtype.
+// part: float32 scratch of k * H * (n_ctx_chunks + n_gen_chunks) * (D + 4).
+// D in {64, 128}; H / Hkv in {1, 2, 4, 8}.
+void decode_attention(int dtype, const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v,
+                      const void* gen_k, const void* gen_v, int64_t ldkv, const DecodeLayout& Ly, int step, int H,
+                      int Hkv, int D, float* part, void* out, int64_t ldo, hipStream_t s);
+
+// Destination of a decode-step projection: `out` with row stride `ldo` (kResidual: float32
+// x += ..., kSwiGLU: bf16 [k, N/2]), or the QKV outputs (kQkvRope, head dim 128).
+struct DecodeEpi {
+    void* out;
+    int64_t ldo;
+    QkvOut qkv;
+};
+
+// K split of the skinny GEMM: `splits` pieces of `tiles_per_split` 128-column tiles.
+struct SkinnySplit {
+    int tiles_per_split, splits;
+};
+SkinnySplit skinny_split(int N, int K);
+// Shapes the skinny GEMM takes: 1 <= k <= 64 rows, N % 64 == 0, K % 128 == 0.
+bool skinny_ok(int k, int N, int K);
+
+// bf16 C = A W^T for k <= 64 rows (A [k, lda], W [N, ldw]) through float32 partial sums
+// (part: splits * k * N floats) and the epilogue `epi` (kResidual, kSwiGLU or kQkvRope).
+void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
+                 const DecodeEpi& ep, hipStream_t s);
+
 }  // namespace ppk

@@ -29,35 +29,6 @@ struct Layout {
 
 size_t elem_size(int dtype) { return dtype == PP_BF16 ? 2 : 4; }
 
-pp_status validate_config(const pp_config* c) {
-    if (!c) return pp::fail(PP_ERR_INVALID_ARG, "config is NULL");
-    if (c->n_layers <= 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
-        c->ffn_dim <= 0 || c->vocab <= 0)
-        return pp::fail(PP_ERR_INVALID_ARG, "config sizes must be positive");
-    if (c->dtype != PP_F32 && c->dtype != PP_BF16) return pp::fail(PP_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
-    if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f))
-        return pp::fail(PP_ERR_INVALID_ARG, "rms_eps must be >= 0 and rope_theta > 0");
-    if (c->n_heads % c->n_kv_heads)
-        return pp::fail(PP_ERR_UNSUPPORTED, "n_heads %d is not a multiple of n_kv_heads %d", c->n_heads,
-                        c->n_kv_heads);
-    if (c->head_dim != 64 && c->head_dim != 128)
-        return pp::fail(PP_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
-    const int64_t qkv_w = int64_t(c->n_heads + 2 * c->n_kv_heads) * c->head_dim;
-    const int64_t hd = int64_t(c->n_heads) * c->head_dim;
-    if (c->dtype == PP_BF16) {
-        if (c->head_dim != 128) return pp::fail(PP_ERR_UNSUPPORTED, "bf16 attention needs head_dim 128");
-        if (c->d_model % 256 || c->ffn_dim % 128 || qkv_w % 256 || hd % 64)
-            return pp::fail(PP_ERR_UNSUPPORTED,
-                            "bf16 GEMM tiles need d %% 256 == 0, F %% 128 == 0, (H+2Hkv)D %% 256 == 0 "
-                            "(d=%d F=%d (H+2Hkv)D=%lld)",
-                            c->d_model, c->ffn_dim, (long long)qkv_w);
-    } else {
-        if (c->d_model % 16 || c->ffn_dim % 16 || hd % 16)
-            return pp::fail(PP_ERR_UNSUPPORTED, "f32 path needs d, F and H*D multiples of 16");
-    }
-    return PP_OK;
-}
-
 // The attention kernel addresses one prompt's cache rows through a 32-bit buffer range.
 pp_status validate_attention_span(const pp_config* c, const pp_dplan* p) {
     const int64_t kvw = int64_t(c->n_kv_heads) * c->head_dim;
@@ -107,6 +78,39 @@ Layout layout_of(const pp_config* c, const pp_dplan* p) {
     return L;
 }
 
+}  // namespace
+
+namespace pp {
+
+pp_status validate_config(const pp_config* c) {
+    if (!c) return pp::fail(PP_ERR_INVALID_ARG, "config is NULL");
+    if (c->n_layers <= 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+        c->ffn_dim <= 0 || c->vocab <= 0)
+        return pp::fail(PP_ERR_INVALID_ARG, "config sizes must be positive");
+    if (c->dtype != PP_F32 && c->dtype != PP_BF16) return pp::fail(PP_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
+    if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f))
+        return pp::fail(PP_ERR_INVALID_ARG, "rms_eps must be >= 0 and rope_theta > 0");
+    if (c->n_heads % c->n_kv_heads)
+        return pp::fail(PP_ERR_UNSUPPORTED, "n_heads %d is not a multiple of n_kv_heads %d", c->n_heads,
+                        c->n_kv_heads);
+    if (c->head_dim != 64 && c->head_dim != 128)
+        return pp::fail(PP_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
+    const int64_t qkv_w = int64_t(c->n_heads + 2 * c->n_kv_heads) * c->head_dim;
+    const int64_t hd = int64_t(c->n_heads) * c->head_dim;
+    if (c->dtype == PP_BF16) {
+        if (c->head_dim != 128) return pp::fail(PP_ERR_UNSUPPORTED, "bf16 attention needs head_dim 128");
+        if (c->d_model % 256 || c->ffn_dim % 128 || qkv_w % 256 || hd % 64)
+            return pp::fail(PP_ERR_UNSUPPORTED,
+                            "bf16 GEMM tiles need d %% 256 == 0, F %% 128 == 0, (H+2Hkv)D %% 256 == 0 "
+                            "(d=%d F=%d (H+2Hkv)D=%lld)",
+                            c->d_model, c->ffn_dim, (long long)qkv_w);
+    } else {
+        if (c->d_model % 16 || c->ffn_dim % 16 || hd % 16)
+            return pp::fail(PP_ERR_UNSUPPORTED, "f32 path needs d, F and H*D multiples of 16");
+    }
+    return PP_OK;
+}
+
 pp_status validate_weights(const pp_config* c, const pp_weights* w) {
     if (!w) return pp::fail(PP_ERR_INVALID_ARG, "weights is NULL");
     if (!w->embed || !w->final_norm || !w->attn_norm || !w->wqkv || !w->wo || !w->mlp_norm || !w->w_gateup ||
@@ -118,7 +122,10 @@ pp_status validate_weights(const pp_config* c, const pp_weights* w) {
     return PP_OK;
 }
 
-}  // namespace
+}  // namespace pp
+
+using pp::validate_config;
+using pp::validate_weights;
 
 extern "C" pp_status pp_prefill_workspace_size(const pp_config* cfg, const pp_dplan* plan, size_t* bytes) {
     pp::clear_error();

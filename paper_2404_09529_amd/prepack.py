@@ -68,6 +68,19 @@ class PPDPlan(ctypes.Structure):
                 ("slot_kv", ctypes.c_void_p), ("qtile_seg", ctypes.c_void_p), ("qtile_q0", ctypes.c_void_p)]
 
 
+class PPGenLayout(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_int32), ("n_new", ctypes.c_int32), ("padded", ctypes.c_int32),
+                ("max_len", ctypes.c_int32), ("ctx_rows", ctypes.c_int64), ("gen_rows", ctypes.c_int64),
+                ("ctx_off", _i32p), ("ctx_span", _i32p), ("ctx_valid", _i32p), ("pos0", _i32p), ("gen_off", _i32p)]
+
+
+class PPGenDLayout(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_int32), ("n_new", ctypes.c_int32), ("padded", ctypes.c_int32),
+                ("max_len", ctypes.c_int32), ("ctx_rows", ctypes.c_int64), ("gen_rows", ctypes.c_int64),
+                ("ctx_off", ctypes.c_void_p), ("ctx_span", ctypes.c_void_p), ("ctx_valid", ctypes.c_void_p),
+                ("pos0", ctypes.c_void_p), ("gen_off", ctypes.c_void_p)]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -101,9 +114,15 @@ def lib() -> ctypes.CDLL:
         L.pp_final_norm_unpack.argtypes = [vp, vp, i32, f32, dpp, vp, vp]
         L.pp_first_token_workspace_size.argtypes = [cfgp, dpp, ctypes.POINTER(ctypes.c_size_t)]
         L.pp_first_token.argtypes = [cfgp, dpp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp]
+        glp, gdp, wp = ctypes.POINTER(PPGenLayout), ctypes.POINTER(PPGenDLayout), ctypes.POINTER(PPWeights)
+        L.pp_gen_layout_make.argtypes = [_i32p, i32, i32, i32, glp]
+        L.pp_decode_workspace_size.argtypes = [cfgp, gdp, ctypes.POINTER(ctypes.c_size_t)]
+        L.pp_decode_step.argtypes = [cfgp, wp, gdp, i32, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp]
+        L.pp_generate.argtypes = [cfgp, wp, gdp, i32, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp, vp]
         for name in ("pp_plan_bounds", "pp_pack", "pp_pack_padded", "pp_prefill_workspace_size", "pp_prefill",
                      "pp_embed", "pp_rmsnorm", "pp_gemm", "pp_rope", "pp_kv_scatter", "pp_attention",
-                     "pp_final_norm_unpack", "pp_first_token_workspace_size", "pp_first_token"):
+                     "pp_final_norm_unpack", "pp_first_token_workspace_size", "pp_first_token",
+                     "pp_gen_layout_make", "pp_decode_workspace_size", "pp_decode_step", "pp_generate"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -373,3 +392,146 @@ def pp_first_token(cfg: PPConfig, dplan: DevicePlan, hidden, lm_head, workspace,
                                 _p(workspace), workspace.numel() * workspace.element_size(), _p(logits),
                                 _p(tokens), _stream(stream)), "pp_first_token")
 
+
+
+# ----------------------------------------------------------------------------- generation
+@dataclass
+class GenLayout:
+    """Host copy of a pp_gen_layout: where each prompt's keys and values live while generating."""
+    k: int
+    n_new: int
+    padded: bool
+    max_len: int
+    ctx_rows: int
+    gen_rows: int
+    ctx_off: np.ndarray
+    ctx_span: np.ndarray
+    ctx_valid: np.ndarray
+    pos0: np.ndarray
+    gen_off: np.ndarray
+
+
+_GEN_ARRAYS = ("ctx_off", "ctx_span", "ctx_valid", "pos0", "gen_off")
+
+
+def pp_gen_layout_make(lengths: Sequence[int], n_new: int, padded: bool = False) -> GenLayout:
+    """Cache layout for generating n_new tokens per prompt: packed, or full batching."""
+    L = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    k = int(L.size)
+    arrs = {n: np.zeros(max(k, 1), dtype=np.int32) for n in _GEN_ARRAYS}
+    g = PPGenLayout(**{n: _ptr(a) for n, a in arrs.items()})
+    _check(lib().pp_gen_layout_make(_ptr(L) if k else None, k, int(n_new), int(bool(padded)), ctypes.byref(g)),
+           "pp_gen_layout_make")
+    return GenLayout(k=g.k, n_new=g.n_new, padded=bool(g.padded), max_len=g.max_len, ctx_rows=g.ctx_rows,
+                     gen_rows=g.gen_rows, **{n: a[:k].copy() for n, a in arrs.items()})
+
+
+class DeviceGenLayout:
+    """A generation layout's arrays in device memory plus the pp_gen_dlayout struct."""
+
+    def __init__(self, layout: GenLayout, device="cuda"):
+        torch = _torch()
+        self.layout = layout
+        self.tensors = {n: torch.from_numpy(getattr(layout, n)).to(device) for n in _GEN_ARRAYS}
+        self.struct = PPGenDLayout(k=layout.k, n_new=layout.n_new, padded=int(layout.padded),
+                                   max_len=layout.max_len, ctx_rows=layout.ctx_rows, gen_rows=layout.gen_rows,
+                                   **{n: t.data_ptr() for n, t in self.tensors.items()})
+
+
+def pp_decode_workspace_size(model: DeviceModel, dlayout: DeviceGenLayout) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().pp_decode_workspace_size(ctypes.byref(model.config), ctypes.byref(dlayout.struct),
+                                          ctypes.byref(n)), "pp_decode_workspace_size")
+    return n.value
+
+
+def pp_decode_step(model: DeviceModel, dlayout: DeviceGenLayout, step: int, tokens_in, lm_head, ctx_k, ctx_v,
+                   gen_k, gen_v, workspace, tokens_out, logits=None, stream=None) -> None:
+    """One greedy decode step of every prompt (see pp_decode_step in include/prepack.h)."""
+    _check(lib().pp_decode_step(ctypes.byref(model.config), ctypes.byref(model.weights_struct),
+                                ctypes.byref(dlayout.struct), int(step), _p(tokens_in), _p(lm_head), _p(ctx_k),
+                                _p(ctx_v), _p(gen_k), _p(gen_v), _p(workspace),
+                                workspace.numel() * workspace.element_size(), _p(logits), _p(tokens_out),
+                                _stream(stream)), "pp_decode_step")
+
+
+def pp_generate(model: DeviceModel, dlayout: DeviceGenLayout, n_steps: int, tokens_first, lm_head, ctx_k, ctx_v,
+                gen_k, gen_v, workspace, tokens, stream=None) -> None:
+    """n_steps greedy decode steps back to back: tokens [n_steps, k] int32."""
+    _check(lib().pp_generate(ctypes.byref(model.config), ctypes.byref(model.weights_struct),
+                             ctypes.byref(dlayout.struct), int(n_steps), _p(tokens_first), _p(lm_head), _p(ctx_k),
+                             _p(ctx_v), _p(gen_k), _p(gen_v), _p(workspace),
+                             workspace.numel() * workspace.element_size(), _p(tokens), _stream(stream)),
+           "pp_generate")
+
+
+class Generation:
+    """Caches and workspace for greedy generation after a prefill (allocated once with torch).
+
+    packed: the prefill's per-prompt caches are the context; the generated keys and values go
+    to a cache of n_new rows per prompt.  padded (full batching): one cache of k rows of
+    m + n_new slots, into which the prefill's caches are placed once at set-up (a copy that
+    is part of building the baseline's layout, not of its decode steps)."""
+
+    def __init__(self, model: DeviceModel, prefill: "Prefill", lengths: Sequence[int], n_new: int,
+                 padded: bool = False, device="cuda"):
+        torch = _torch()
+        s = model.shape
+        self.model, self.n_new, self.padded = model, int(n_new), bool(padded)
+        self.layout = pp_gen_layout_make(lengths, n_new, padded)
+        self.dlayout = DeviceGenLayout(self.layout, device)
+        kvw = s.n_kv_heads * s.head_dim
+        rows = (s.n_layers, self.layout.gen_rows, kvw)
+        if padded:
+            self.gen_k = torch.zeros(rows, dtype=model.torch_dtype, device=device)
+            self.gen_v = torch.zeros(rows, dtype=model.torch_dtype, device=device)
+            lay = self.layout
+            dest = np.concatenate([lay.ctx_off[i] + np.arange(lay.ctx_valid[i]) for i in range(lay.k)])
+            idx = torch.from_numpy(dest.astype(np.int64)).to(device)
+            self.gen_k.index_copy_(1, idx, prefill.k_cache)
+            self.gen_v.index_copy_(1, idx, prefill.v_cache)
+            self.ctx_k, self.ctx_v = self.gen_k, self.gen_v
+        else:
+            self.ctx_k, self.ctx_v = prefill.k_cache, prefill.v_cache
+            self.gen_k = torch.empty(rows, dtype=model.torch_dtype, device=device)
+            self.gen_v = torch.empty(rows, dtype=model.torch_dtype, device=device)
+        self.workspace = torch.empty(max(pp_decode_workspace_size(model, self.dlayout), 1), dtype=torch.uint8,
+                                     device=device)
+        self.tokens = torch.empty((self.n_new, self.layout.k), dtype=torch.int32, device=device)
+
+    def kv_cache_bytes(self) -> int:
+        """Bytes of key/value cache this layout holds for the whole generation."""
+        t = [self.gen_k, self.gen_v] + ([] if self.padded else [self.ctx_k, self.ctx_v])
+        return int(sum(x.numel() * x.element_size() for x in t))
+
+    def step(self, step: int, tokens_in, lm_head, tokens_out, logits=None, stream=None) -> None:
+        pp_decode_step(self.model, self.dlayout, step, tokens_in, lm_head, self.ctx_k, self.ctx_v, self.gen_k,
+                       self.gen_v, self.workspace, tokens_out, logits, stream)
+
+    def __call__(self, tokens_first, lm_head, n_steps: Optional[int] = None, stream=None):
+        n = self.n_new if n_steps is None else n_steps
+        pp_generate(self.model, self.dlayout, n, tokens_first, lm_head, self.ctx_k, self.ctx_v, self.gen_k,
+                    self.gen_v, self.workspace, self.tokens, stream)
+        return self.tokens[:n]
+
+    def capture(self, tokens_first, lm_head, n_steps: Optional[int] = None):
+        """Record the whole pp_generate call (every launch of every step) into a HIP graph
+        with torch's graph capture; replay() then re-runs it with one launch from the host.
+        The graph is bound to these buffers, tokens_first and lm_head included: refill
+        tokens_first in place before a replay to generate from new first tokens."""
+        torch = _torch()
+        n = self.n_new if n_steps is None else n_steps
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):             # warm-up off the capture, as torch requires
+            self(tokens_first, lm_head, n)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self(tokens_first, lm_head, n)
+        return self.tokens[:n]
+
+    def replay(self):
+        self.graph.replay()
+        return self.tokens

@@ -259,3 +259,103 @@ def test_first_token_workspace_and_rejections(L):
     assert call(p=_dplan(total_len=1)) == pp.PP_ERR_INVALID_ARG   # fewer tokens than prompts
     assert call(c=_cfg(vocab=0)) == pp.PP_ERR_INVALID_ARG
     assert call(p=_dplan(k=0, total_len=0)) == pp.PP_OK            # no prompt: nothing to do
+
+
+# ----------------------------------------------------------------------------- generation
+def test_gen_layout_packed_and_padded_by_hand(L):
+    """pp_gen_layout_make on lengths 3, 1, 5 with room for 4 new tokens."""
+    p = pp.pp_gen_layout_make([3, 1, 5], 4)
+    assert (p.k, p.n_new, p.padded, p.max_len, p.ctx_rows, p.gen_rows) == (3, 4, False, 5, 9, 12)
+    assert p.ctx_off.tolist() == [0, 3, 4] and p.ctx_span.tolist() == [3, 1, 5]
+    assert p.ctx_valid.tolist() == [3, 1, 5] and p.pos0.tolist() == [3, 1, 5] and p.gen_off.tolist() == [0, 4, 8]
+    f = pp.pp_gen_layout_make([3, 1, 5], 4, padded=True)
+    assert (f.ctx_rows, f.gen_rows, f.max_len) == (27, 27, 5)   # 3 rows of 5 + 4 slots
+    assert f.ctx_off.tolist() == [0, 9, 18] and f.ctx_span.tolist() == [5, 5, 5]
+    assert f.ctx_valid.tolist() == [3, 1, 5] and f.gen_off.tolist() == [5, 14, 23]
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.lists(st.integers(1, 300), min_size=1, max_size=40), st.integers(1, 64), st.booleans())
+def test_gen_layout_rows_are_disjoint_and_in_range(lengths, n_new, padded):
+    """Every key row any decode step reads or writes lies inside its cache, and no two prompts
+    (nor a prompt's context and generated rows in the padded layout) share a row."""
+    g = pp.pp_gen_layout_make(lengths, n_new, padded)
+    used_ctx, used_gen = set(), set()
+    for i, l in enumerate(lengths):
+        ctx = set(range(g.ctx_off[i], g.ctx_off[i] + g.ctx_span[i]))
+        gen = set(range(g.gen_off[i], g.gen_off[i] + n_new))
+        assert g.ctx_valid[i] == l and g.pos0[i] == l and g.ctx_span[i] >= l
+        assert min(ctx) >= 0 and max(ctx) < g.ctx_rows and min(gen) >= 0 and max(gen) < g.gen_rows
+        assert not (ctx & used_ctx) and not (gen & used_gen)
+        if padded:
+            assert not (ctx & gen) and not (gen & used_ctx) and not (ctx & used_gen)
+        used_ctx |= ctx
+        used_gen |= gen
+    if not padded:   # packed: the context is exactly the prefill's compact cache, nothing padded
+        assert g.ctx_rows == sum(lengths) and len(used_ctx) == sum(lengths) and g.gen_rows == len(lengths) * n_new
+
+
+def test_gen_layout_rejections(L):
+    with pytest.raises(pp.PrepackError):
+        pp.pp_gen_layout_make([3, 0], 4)
+    with pytest.raises(pp.PrepackError):
+        pp.pp_gen_layout_make([3], 0)
+    with pytest.raises(pp.PrepackError):
+        pp.pp_gen_layout_make([], 4)
+    with pytest.raises(pp.PrepackError):
+        pp.pp_gen_layout_make([1 << 20] * 3000, 4, padded=True)   # more rows than an int32 index
+
+
+def _glayout(**kw):
+    base = dict(k=3, n_new=8, padded=0, max_len=300, ctx_rows=500, gen_rows=24,
+                **{n: 0x1000 for n in ("ctx_off", "ctx_span", "ctx_valid", "pos0", "gen_off")})
+    base.update(kw)
+    return pp.PPGenDLayout(**base)
+
+
+def test_decode_workspace_and_rejections(L):
+    """Workspace size of the decode step and every host-side check of pp_decode_step and
+    pp_generate: they return before any launch, so no GPU is needed."""
+    cfg, gl = _cfg(vocab=32000), _glayout()
+    n = ctypes.c_size_t()
+    assert L.pp_decode_workspace_size(ctypes.byref(cfg), ctypes.byref(gl), ctypes.byref(n)) == pp.PP_OK
+    k, d, H, D, F = 3, 4096, 32, 128, 14336
+    chunks = 2 + 1                                          # ceil(300 / 256) context + 1 generated
+    want = (k * d * 4 + k * d * 2 + k * H * D * 2 + k * H * D * 2 + k * F * 2 + k * d * 4
+            + k * H * chunks * (D + 4) * 4 + k * 64 * 8 + (4 * k + 1) * 4 + 16 * d * 2 + 250 * k * 8)
+    assert want <= n.value <= want + 12 * 256
+    ws = n.value
+    bad = lambda **kw: L.pp_decode_workspace_size(ctypes.byref(cfg), ctypes.byref(_glayout(**kw)),
+                                                  ctypes.byref(n))
+    assert bad(k=0) == pp.PP_ERR_INVALID_ARG
+    assert bad(n_new=0) == pp.PP_ERR_INVALID_ARG
+    assert bad(padded=2) == pp.PP_ERR_INVALID_ARG
+    assert bad(gen_rows=23) == pp.PP_ERR_INVALID_ARG         # fewer than k * n_new rows
+    assert bad(gen_off=0) == pp.PP_ERR_INVALID_ARG           # NULL device array
+    odd = _cfg(n_heads=24, n_kv_heads=8, vocab=32000)        # 3 query heads per key/value head
+    assert L.pp_decode_workspace_size(ctypes.byref(odd), ctypes.byref(gl), ctypes.byref(n)) == pp.PP_ERR_UNSUPPORTED
+    w, keep = _weights(1)
+    f = L.pp_decode_step
+    ok = dict(step=0, tin=0x3000, lm=0x4000, ck=0x5000, cv=0x6000, gk=0x7000, gv=0x8000, ws=0x10000, nb=ws,
+              tout=0x9000)
+    def call(c=cfg, g=gl, **kw):
+        a = {**ok, **kw}
+        return f(ctypes.byref(c), ctypes.byref(w), ctypes.byref(g), a["step"], a["tin"], a["lm"], a["ck"], a["cv"],
+                 a["gk"], a["gv"], a["ws"], a["nb"], None, a["tout"], None)
+    assert call(step=8) == pp.PP_ERR_INVALID_ARG             # step outside [0, n_new)
+    assert call(step=-1) == pp.PP_ERR_INVALID_ARG
+    assert call(tin=None) == pp.PP_ERR_INVALID_ARG
+    assert call(tout=None) == pp.PP_ERR_INVALID_ARG
+    assert call(gk=None) == pp.PP_ERR_INVALID_ARG
+    assert call(lm=None) == pp.PP_ERR_INVALID_ARG
+    assert call(ws=0x10008) == pp.PP_ERR_INVALID_ARG         # misaligned workspace
+    assert call(nb=ws - 1) == pp.PP_ERR_BUFFER_TOO_SMALL
+    assert call(c=_cfg(head_dim=96, vocab=32000)) == pp.PP_ERR_UNSUPPORTED
+    g = L.pp_generate
+    gen = lambda steps, **kw: g(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(gl), steps, 0x3000, 0x4000,
+                                0x5000, 0x6000, 0x7000, 0x8000, kw.get("ws", 0x10000), kw.get("nb", ws), 0x9000,
+                                None)
+    assert gen(9) == pp.PP_ERR_INVALID_ARG                   # more steps than the caches hold
+    assert gen(-1) == pp.PP_ERR_INVALID_ARG
+    assert gen(0) == pp.PP_OK                                # nothing to do
+    assert gen(4, nb=ws - 256) == pp.PP_ERR_BUFFER_TOO_SMALL

@@ -1,0 +1,224 @@
+"""Greedy generation with packed KV caches on the GPU (section 4.8), through the C ABI,
+against the generation oracle (full recomputation per token, section 2.2).
+
+* float32 model: pp_generate's tokens equal the oracle's wherever the oracle's choice is
+  clear (best logit ahead of the second by more than 1e-3; float32 errors are ~1e-6), and
+  the generated cache rows meet the stated bar (2e-2 / 2e-3).
+* bf16 models, teacher-forced (up to 64 prompts the projections take the split-K GEMM for
+  one row per prompt, beyond that the prefill's tiled GEMMs): every pp_decode_step is fed
+  the oracle's token, and the rows
+  it appends to the cache and its logits are gated against the error of an ideal bf16
+  pipeline (the oracle with every stored value rounded to bf16), as the prefill's parity
+  is; its token must be the oracle's where the oracle's lead exceeds twice the logit error,
+  else a valid argmax.
+* the packed and the full-batching layouts give bit-identical tokens and generated rows,
+  and pp_generate is bit-identical to the same steps taken one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as D
+from oracle import generate as G
+from paper_2404_09529_amd import prepack as pp
+from paper_2404_09529_amd import workloads as W
+
+from .gpu_util import bf16_dev, f32_dev, host64, i32_dev, report, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+BAR_MAX, BAR_MEAN = 2e-2, 2e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _prefill(case, lm_head):
+    """GPU prefill (packed, bin size = longest prompt) and first token of every prompt."""
+    model = pp.DeviceModel(case.shape, case.weights)
+    dplan = pp.DevicePlan(pp.pp_pack(case.lengths, 0))
+    pre = pp.Prefill(model, dplan)
+    pre(i32_dev(case.tokens))
+    lm = bf16_dev(lm_head) if case.shape.dtype == "bf16" else f32_dev(lm_head)
+    ws = torch.empty(max(pp.pp_first_token_workspace_size(model.config, dplan), 1), dtype=torch.uint8,
+                     device="cuda")
+    first = torch.empty(len(case.lengths), dtype=torch.int32, device="cuda")
+    pp.pp_first_token(model.config, dplan, pre.hidden, lm, ws, first)
+    return model, pre, lm, first
+
+
+def _prompts(case):
+    off = np.concatenate([[0], np.cumsum(case.lengths)])
+    return [case.tokens[off[i]:off[i + 1]] for i in range(len(case.lengths))]
+
+
+def _gen_rows(gen, layer, i, n, which="k"):
+    t = gen.gen_k if which == "k" else gen.gen_v
+    r = int(gen.layout.gen_off[i])
+    return host64(t[layer, r:r + n])
+
+
+def _gap(logits):
+    s = np.sort(logits)
+    return s[-1] - s[-2]
+
+
+# ----------------------------------------------------------------------------- float32: tokens and the bar
+@pytest.mark.parametrize("lengths,n_new,n_layers", [
+    ([5, 1, 17, 9, 40], 6, 2),
+    ([1], 1, 1),                      # one prompt of one token, one step
+    ([3] * 70, 3, 1),                 # more than 64 prompts (two LM-head prompt chunks)
+    ([290, 30], 260, 1),              # over 256 context keys and over 256 generated keys
+])
+def test_fp32_generate_matches_oracle(lengths, n_new, n_layers):
+    case = W.make_case(1, 3, n_layers=n_layers, lengths=lengths, random_gains=True)
+    lm_head = W.draw_lm_head(case.wl, 3, case.shape)
+    sh = D.Shape.of(case.shape)
+    print(f"[generate] f32 lengths {lengths[:6]} (k={len(lengths)}) n_new {n_new}", flush=True)
+    model, pre, lm, first = _prefill(case, lm_head)
+    gen = pp.Generation(model, pre, case.lengths, n_new)
+    toks = gen(first, lm)
+    torch.cuda.synchronize()
+    got = np.concatenate([first.cpu().numpy()[None], toks.cpu().numpy()]).T     # [k, 1 + n_new]
+    picks = range(len(lengths)) if len(lengths) <= 8 else [0, 33, 69]
+    for i in picks:
+        p = _prompts(case)[i]
+        ref = G.generate(p, case.weights, sh, lm_head, n_new + 1)
+        f = G.teacher_forced(p, ref[:-1], case.weights, sh, lm_head)
+        gaps = [_gap(D.prefill_prompt(p, case.weights, sh).hidden[-1] @ lm_head.T)] + [_gap(r) for r in f.logits]
+        clear = next((t for t, g in enumerate(gaps) if g <= 1e-3), len(gaps))
+        assert got[i][:clear].tolist() == ref[:clear].tolist(), (i, got[i].tolist(), ref.tolist())
+        if clear == len(gaps):   # same tokens fed: the generated rows compare one to one
+            for l in range(n_layers):
+                for which, ref_rows in (("k", f.k[l]), ("v", f.v[l])):
+                    mx, mean = report(f"f32 prompt {i} {which}{l}", _gen_rows(gen, l, i, n_new, which), ref_rows)
+                    assert mx <= BAR_MAX and mean <= BAR_MEAN
+
+
+# ----------------------------------------------------------------------------- bf16, teacher-forced
+def _bf16_case(model_name, lengths, n_layers, seed=0):
+    s = W.MODELS[model_name]
+    return W.make_case(6, seed, lengths=lengths, random_gains=True, n_layers=n_layers, d_model=s.d_model,
+                       n_heads=s.n_heads, n_kv_heads=s.n_kv_heads, ffn_dim=s.ffn_dim)
+
+
+@pytest.mark.parametrize("model_name,lengths,n_layers,n_new", [
+    ("llama-1.3b", [37, 1, 300, 5, 129], 2, 4),
+    ("mistral-7b", [64, 260, 3], 1, 3),
+    ("llama-1.3b", [3] * 62 + [40, 9, 300, 1, 2, 7, 5, 3], 1, 2),   # over 64 prompts: the tiled GEMMs
+])
+def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
+    case = _bf16_case(model_name, lengths, n_layers)
+    lm_head = W.draw_lm_head(case.wl, 0, case.shape)
+    sh = D.Shape.of(case.shape)
+    k, V = len(lengths), case.shape.vocab
+    print(f"[generate] bf16 {model_name} lengths {lengths} layers {n_layers} n_new {n_new}", flush=True)
+    model, pre, lm, _ = _prefill(case, lm_head)
+    gen = pp.Generation(model, pre, case.lengths, n_new)
+    prompts = _prompts(case)
+    fed = np.stack([G.generate(p, case.weights, sh, lm_head, n_new + 1) for p in prompts])   # oracle's greedy
+    ref = [G.teacher_forced(p, fed[i, :n_new], case.weights, sh, lm_head) for i, p in enumerate(prompts)]
+    flo = [G.teacher_forced(p, fed[i, :n_new], case.weights, sh, lm_head, rnd=D.round_bf16)
+           for i, p in enumerate(prompts)]
+    logits = torch.empty((k, V), dtype=torch.float32, device="cuda")
+    out = torch.empty(k, dtype=torch.int32, device="cuda")
+    for t in range(n_new):
+        gen.step(t, i32_dev(fed[:, t]), lm, out, logits)
+        lg = host64(logits)
+        tok = out.cpu().numpy()
+        for i in range(k):
+            want, floor = ref[i].logits[t], flo[i].logits[t]
+            err = np.abs(lg[i] - want)
+            ferr = np.abs(floor - want)
+            assert err.mean() <= 1.5 * ferr.mean() + 1e-4 and err.max() <= 2 * ferr.max() + 1e-3, \
+                (t, i, err.max(), err.mean(), ferr.max(), ferr.mean())
+            slack = 2 * err.max()
+            top = np.sort(want)[::-1]
+            if top[0] - top[1] > slack:
+                assert tok[i] == fed[i, t + 1], (t, i, tok[i], fed[i, t + 1])
+            else:
+                assert want[tok[i]] >= top[0] - slack
+    for l in range(n_layers):
+        for which in ("k", "v"):
+            errs = []
+            for i in range(k):
+                got = _gen_rows(gen, l, i, n_new, which)
+                want = (ref[i].k if which == "k" else ref[i].v)[l]
+                floor = (flo[i].k if which == "k" else flo[i].v)[l]
+                (gm, ga), (fm, fa) = D.errors(got, want), D.errors(floor, want)
+                errs.append((gm, ga, fm, fa))
+            gm, ga = max(e[0] for e in errs), np.mean([e[1] for e in errs])
+            fm, fa = max(e[2] for e in errs), np.mean([e[3] for e in errs])
+            print(f"[parity] {model_name} generated {which}{l}: max {gm:.3e} mean {ga:.3e} "
+                  f"(bf16 floor {fm:.3e} / {fa:.3e})", flush=True)
+            assert ga <= 1.5 * fa + 1e-4 and gm <= 2 * fm + 1e-3
+
+
+# ----------------------------------------------------------------------------- layouts and entry points agree
+@pytest.mark.parametrize("model_name,lengths,n_layers", [
+    ("llama-1.3b", [1, 300, 7, 129, 1, 64], 1),
+    ("mistral-7b", [700, 2, 33], 1),
+])
+def test_packed_and_padded_generation_are_bit_identical(model_name, lengths, n_layers):
+    case = _bf16_case(model_name, lengths, n_layers, seed=1)
+    lm_head = W.draw_lm_head(case.wl, 1, case.shape)
+    n_new = 5
+    model, pre, lm, first = _prefill(case, lm_head)
+    packed = pp.Generation(model, pre, case.lengths, n_new)
+    padded = pp.Generation(model, pre, case.lengths, n_new, padded=True)
+    a = packed(first, lm).cpu().numpy()
+    b = padded(first, lm).cpu().numpy()
+    torch.cuda.synchronize()
+    assert np.array_equal(a, b)
+    for l in range(n_layers):
+        for i in range(len(lengths)):
+            for which in ("k", "v"):
+                assert np.array_equal(_gen_rows(packed, l, i, n_new, which), _gen_rows(padded, l, i, n_new, which))
+    # the full-batching cache is larger by the padding of every prompt to the longest
+    assert padded.kv_cache_bytes() > packed.kv_cache_bytes()
+
+
+def test_generate_equals_steps_one_by_one():
+    case = _bf16_case("llama-1.3b", [9, 200, 1], 2, seed=2)
+    lm_head = W.draw_lm_head(case.wl, 2, case.shape)
+    n_new = 4
+    model, pre, lm, first = _prefill(case, lm_head)
+    whole = pp.Generation(model, pre, case.lengths, n_new)
+    toks = whole(first, lm).clone()
+    steps = pp.Generation(model, pre, case.lengths, n_new)
+    prev = first
+    outs = []
+    for t in range(n_new):
+        out = torch.empty_like(first)
+        steps.step(t, prev, lm, out)
+        outs.append(out)
+        prev = out
+    torch.cuda.synchronize()
+    assert np.array_equal(toks.cpu().numpy(), torch.stack(outs).cpu().numpy())
+    for l in range(2):
+        assert torch.equal(whole.gen_k[l], steps.gen_k[l]) and torch.equal(whole.gen_v[l], steps.gen_v[l])
+
+
+def test_graph_replays_match_eager_generation():
+    """The whole generation captured as one HIP graph: every replay, with eager work and
+    synchronisations between replays, gives the eager call's tokens and generated rows."""
+    case = _bf16_case("llama-1.3b", [11, 1, 130, 4], 2, seed=4)
+    lm_head = W.draw_lm_head(case.wl, 4, case.shape)
+    model, pre, lm, first = _prefill(case, lm_head)
+    eager = pp.Generation(model, pre, case.lengths, 6)
+    want = eager(first, lm).clone()
+    torch.cuda.synchronize()
+    g = pp.Generation(model, pre, case.lengths, 6)
+    g.capture(first, lm)
+    for rep in range(3):
+        g.gen_k.zero_()
+        g.tokens.fill_(-5)
+        torch.cuda.synchronize()
+        got = g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(got, want), rep
+        assert torch.equal(g.gen_k, eager.gen_k) and torch.equal(g.gen_v, eager.gen_v), rep
+        eager(first, lm)                       # eager work between replays
+        torch.cuda.synchronize()
