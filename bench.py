@@ -172,11 +172,14 @@ def batch_predictors(lengths, n_rows):
 
 
 def linear_fit(x, y):
-    """Ordinary least squares y ~ a + b x: slope b, intercept a, Pearson correlation and R^2."""
+    """Ordinary least squares y ~ a + b x: slope b, intercept a, Pearson correlation and R^2;
+    None when x or y does not vary (a batch size of 1 has r/k = 1 for every batch)."""
     import numpy as np
     x, y = np.asarray(x, dtype=np.float64), np.asarray(y, dtype=np.float64)
     xm, ym = x.mean(), y.mean()
     sxx, syy, sxy = np.sum((x - xm) ** 2), np.sum((y - ym) ** 2), np.sum((x - xm) * (y - ym))
+    if sxx == 0 or syy == 0:
+        return None
     b = sxy / sxx
     r = sxy / np.sqrt(sxx * syy)
     return {"slope": float(b), "intercept": float(ym - b * xm), "pearson_r": float(r), "r2": float(r * r),
@@ -368,9 +371,16 @@ def run_generate(args):
         t = time_steps(lambda: gen(first, lm, stream=stream), args.reps, args.sweep_warmup)
         torch.cuda.synchronize()
         toks[name] = gen.tokens.cpu().numpy()
+        gen.capture(first, lm)                 # the same call recorded as one HIP graph
+        tg = time_steps(gen.replay, args.reps, args.sweep_warmup)
+        torch.cuda.synchronize()
+        graph_same = bool(np.array_equal(gen.tokens.cpu().numpy(), toks[name]))
         nbytes = decode_step_bytes(shape, lengths, n_new, padded)
         ms = t["ms_median"]
+        mg = tg["ms_median"]
         out[name] = {"ms": ms, "ms_per_token": ms / n_new, "ms_p10": t["ms_p10"], "ms_p90": t["ms_p90"],
+                     "graph_ms": mg, "graph_ms_per_token": mg / n_new, "graph_tokens_identical": graph_same,
+                     "graph_roofline_frac": round(nbytes / (mg / 1e3) / 1e9 / PEAK_HBM_GBPS, 4),
                      "kv_cache_bytes": gen.kv_cache_bytes(),
                      "peak_alloc_bytes": int(torch.cuda.max_memory_allocated()),
                      "extra_alloc_bytes": int(torch.cuda.max_memory_allocated() - base_alloc),
@@ -378,13 +388,15 @@ def run_generate(args):
                      "roofline": {"bound": "hbm", "achieved": round(nbytes / (ms / 1e3) / 1e9, 1),
                                   "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                                   "frac": round(nbytes / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS, 4)}}
-        log(f"{name}: {ms:.3f} ms for {n_new} tokens ({ms / n_new:.3f} ms/token), KV cache "
+        log(f"{name}: {ms:.3f} ms for {n_new} tokens ({ms / n_new:.3f} ms/token; as one HIP graph "
+            f"{mg:.3f} ms, {nbytes / (mg / 1e3) / 1e9:.0f} GB/s), KV cache "
             f"{gen.kv_cache_bytes() / 1e6:.1f} MB, peak {torch.cuda.max_memory_allocated() / 1e9:.2f} GB, "
             f"{nbytes / (ms / 1e3) / 1e9:.0f} GB/s algorithmic")
         del gen
         torch.cuda.empty_cache()
     out["tokens_identical"] = bool(np.array_equal(toks["packed"], toks["padded"]))
     out["time_saving"] = 1.0 - out["packed"]["ms"] / out["padded"]["ms"]
+    out["graph_time_saving"] = 1.0 - out["packed"]["graph_ms"] / out["padded"]["graph_ms"]
     out["kv_memory_saving"] = 1.0 - out["packed"]["kv_cache_bytes"] / out["padded"]["kv_cache_bytes"]
     out["peak_memory_saving"] = 1.0 - out["packed"]["peak_alloc_bytes"] / out["padded"]["peak_alloc_bytes"]
     print(json.dumps(out), flush=True)
@@ -455,8 +467,10 @@ def run_sweep(args):
                               "ttft_ms_padded_mean": float(td.mean()), "ttft_ms_padded_std": float(td.std()),
                               "ttft_speedup_mean": float(col("ttft_speedup").mean())})
             if n_b >= 3:
-                entry["fit_r_over_k"] = linear_fit(col("r_over_k"), sp)
-                entry["fit_max_abs_dev"] = linear_fit(col("max_abs_dev"), sp)
+                for key, x in (("fit_r_over_k", "r_over_k"), ("fit_max_abs_dev", "max_abs_dev")):
+                    fit = linear_fit(col(x), sp)
+                    if fit is not None:
+                        entry[key] = fit
             if args.sweep == "regression":
                 entry["records"] = recs
             out["per_batch_size"].append(entry)

@@ -9,7 +9,8 @@
 //   per layer: rmsnorm -> QKV projection with RoPE and the append to the generation cache
 //              (bf16: the prefill's fused epilogue; float32: GEMM, RoPE, scatter) ->
 //              split-key decode attention + combine -> O GEMM (+residual) -> rmsnorm ->
-//              gate/up GEMM with SwiGLU -> down GEMM (+residual)
+//              gate/up GEMM with SwiGLU -> down GEMM (+residual); with the split-K GEMMs
+//              the residual adds of O and down happen in the norm that follows each
 //   final rmsnorm (float32) -> LM head and greedy choice (the first-token kernels, one
 //   row per prompt).
 // The projections: for bf16 steps of up to 64 prompts, the skinny split-K GEMM with its
@@ -31,8 +32,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 size_t elem_size(int dtype) { return dtype == PP_BF16 ? 2 : 4; }
 
 struct Layout {
-    size_t x = 0, xn = 0, q = 0, attn = 0, act = 0, gu = 0, h = 0, part = 0, table = 0, ints = 0, ft = 0, gpart = 0,
-           total = 0;
+    size_t x = 0, xn = 0, q = 0, attn = 0, act = 0, gu = 0, h = 0, part = 0, table = 0, ints = 0, counters = 0,
+           ft = 0, gpart = 0, total = 0;
 };
 
 // The projections of a decode step as (N, K).
@@ -47,9 +48,9 @@ void projections(const pp_config* c, Proj (&p)[4]) {
     p[3] = {d, c->ffn_dim};                                       // down
 }
 
-// bf16 steps of up to 64 prompts take the skinny GEMM for every projection.
+// bf16 steps of up to 64 prompts (d <= 4096) take the skinny GEMM for every projection.
 bool use_skinny(const pp_config* c, int k) {
-    if (c->dtype != PP_BF16) return false;
+    if (c->dtype != PP_BF16 || c->d_model > 4096) return false;   // d: the fused residual norm's limit
     Proj p[4];
     projections(c, p);
     for (const Proj& q : p)
@@ -58,6 +59,15 @@ bool use_skinny(const pp_config* c, int k) {
 }
 
 int chunks(int n) { return (n + ppk::kDecodeChunk - 1) / ppk::kDecodeChunk; }
+
+// Row-group counters of the split-K projections (one array, reused by every projection).
+int n_counters(const pp_config* c) {
+    Proj p[4];
+    projections(c, p);
+    int n = 0;
+    for (const Proj& q : p) n = std::max(n, q.N % 64 == 0 ? ppk::skinny_counters(q.N) : 0);
+    return n;
+}
 
 Layout layout_of(const pp_config* c, const pp_gen_dlayout* g) {
     const size_t k = g->k, e = elem_size(c->dtype);
@@ -81,6 +91,7 @@ Layout layout_of(const pp_config* c, const pp_gen_dlayout* g) {
     L.part = take(k * size_t(c->n_heads) * nch * (D + 4) * 4);
     L.table = take(k * (D / 2) * sizeof(float2));
     L.ints = take((4 * k + 1) * sizeof(int32_t));
+    L.counters = take(size_t(n_counters(c)) * sizeof(int32_t));
     L.ft = take(ppk::first_token_workspace(c->dtype, g->k, c->vocab, c->d_model));
     size_t gpart = 0;
     if (use_skinny(c, g->k)) {
@@ -157,26 +168,40 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
     int32_t* slot_kv = slot_pos + k;
     int32_t* slot_seg = slot_kv + k;
     int32_t* ident = slot_seg + k;        // k + 1 entries
+    int32_t* counters = reinterpret_cast<int32_t*>(ws + L.counters);
+    const int nc = n_counters(cfg);
     const size_t ctx_layer = size_t(g->ctx_rows) * kvw * e, gen_layer = size_t(g->gen_rows) * kvw * e;
     const ppk::DecodeLayout Ly{k, chunks(g->max_len), chunks(g->n_new), g->ctx_off, g->ctx_span, g->ctx_valid,
                                g->pos0, g->gen_off};
     const bool skinny = use_skinny(cfg, k);
     float* gpart = reinterpret_cast<float*>(ws + L.gpart);
 
-    ppk::decode_prep(Ly, step, D, cfg->rope_theta, table, slot_pos, slot_kv, slot_seg, ident, s);
+    // the split-K residual projections (O, down) leave their partial sums in gpart; the next
+    // norm adds them to x (pending = their split count) before normalising
+    int pending = 0;
+    auto norm = [&](const float* gain, void* out, int out_dtype) {
+        if (skinny)
+            ppk::residual_rmsnorm(out_dtype, x, gpart, pending, k, d, gain, out, eps, s);
+        else
+            ppk::rmsnorm(out_dtype, x, gain, out, k, d, eps, s);
+        pending = 0;
+    };
+    ppk::decode_prep(Ly, step, D, cfg->rope_theta, table, slot_pos, slot_kv, slot_seg, ident, counters, nc, s);
     ppk::embed(dt, x, w->embed, cfg->vocab, tokens_in, ident, k, d, s);
     for (int l = 0; l < cfg->n_layers; ++l) {
         const void* ck = static_cast<const char*>(ctx_k) + l * ctx_layer;
         const void* cv = static_cast<const char*>(ctx_v) + l * ctx_layer;
         void* gk = static_cast<char*>(gen_k) + l * gen_layer;
         void* gv = static_cast<char*>(gen_v) + l * gen_layer;
-        ppk::rmsnorm(dt, x, w->attn_norm[l], xn, k, d, eps, s);
+        norm(w->attn_norm[l], xn, dt);
         if (skinny) {
             const ppk::QkvOut qo{q, hd, gk, gv, kvw, table, slot_pos, slot_kv, H, Hkv};
-            ppk::decode_gemm(ppk::kQkvRope, xn, d, k, w->wqkv[l], d, qkv_w, d, gpart, ppk::DecodeEpi{nullptr, 0, qo},
-                             s);
+            ppk::decode_gemm(ppk::kQkvRope, xn, d, k, w->wqkv[l], d, qkv_w, d, gpart, counters,
+                             ppk::DecodeEpi{nullptr, 0, qo}, s);
             ppk::decode_attention(dt, q, hd, ck, cv, gk, gv, kvw, Ly, step, H, Hkv, D, part, attn, hd, s);
-            ppk::decode_gemm(ppk::kResidual, attn, hd, k, w->wo[l], hd, d, hd, gpart, ppk::DecodeEpi{x, d, qo}, s);
+            ppk::decode_gemm(ppk::kResidual, attn, hd, k, w->wo[l], hd, d, hd, gpart, counters, ppk::DecodeEpi{x, d, qo},
+                             s);
+            pending = ppk::skinny_split(d, hd).splits;
         } else if (bf) {
             const ppk::QkvOut qo{q, hd, gk, gv, kvw, table, slot_pos, slot_kv, H, Hkv};
             ppk::qkv_rope_bf16(xn, d, w->wqkv[l], d, k, d, slot_seg, k, qo, s);
@@ -192,12 +217,14 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
             ppk::gemm_f32(ppk::kResidual, static_cast<const float*>(attn), hd, static_cast<const float*>(w->wo[l]),
                           hd, x, d, k, d, hd, s);
         }
-        ppk::rmsnorm(dt, x, w->mlp_norm[l], xn, k, d, eps, s);
+        norm(w->mlp_norm[l], xn, dt);
         if (skinny) {
             const ppk::QkvOut none{};
-            ppk::decode_gemm(ppk::kSwiGLU, xn, d, k, w->w_gateup[l], d, 2 * F, d, gpart, ppk::DecodeEpi{act, F, none},
-                             s);
-            ppk::decode_gemm(ppk::kResidual, act, F, k, w->w_down[l], F, d, F, gpart, ppk::DecodeEpi{x, d, none}, s);
+            ppk::decode_gemm(ppk::kSwiGLU, xn, d, k, w->w_gateup[l], d, 2 * F, d, gpart, counters,
+                             ppk::DecodeEpi{act, F, none}, s);
+            ppk::decode_gemm(ppk::kResidual, act, F, k, w->w_down[l], F, d, F, gpart, counters,
+                             ppk::DecodeEpi{x, d, none}, s);
+            pending = ppk::skinny_split(d, F).splits;
         } else if (bf) {
             ppk::gemm_bf16(ppk::kSwiGLU, xn, d, w->w_gateup[l], d, act, F, k, 2 * F, d, nullptr, 0, s);
             ppk::gemm_bf16(ppk::kResidual, act, F, w->w_down[l], F, x, d, k, d, F, nullptr, 0, s);
@@ -209,7 +236,7 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
                           F, x, d, k, d, F, s);
         }
     }
-    ppk::rmsnorm(PP_F32, x, w->final_norm, h, k, d, eps, s);
+    norm(w->final_norm, h, PP_F32);
     ppk::first_token(dt, h, ident, k, lm_head, cfg->vocab, d, ws + L.ft, logits, tokens_out, s);
 }
 

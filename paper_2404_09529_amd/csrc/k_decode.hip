@@ -10,20 +10,21 @@
 // decode_attn_kernel     split-key attention of one query row per prompt against that
 //                        prompt's keys only: context rows (its prompt tokens, plus masked
 //                        padding in the full-batching layout) and the generated rows so far.
-//                        A workgroup takes one (prompt, key/value head, chunk of 256 keys)
+//                        A workgroup takes one (prompt, key/value head, chunk of 128 keys)
 //                        and all query heads of the group, so every key and value is read
 //                        from HBM once per step; it writes the chunk's (max, sum, output).
 // decode_combine_kernel  merges a prompt's chunk results in a fixed order.
 // skinny_gemm_kernel     the projections of a decode step, one row per prompt (k <= 64):
 //                        C[k, N] = A[k, K] W[N, K]^T is bound by streaming W from HBM, so
-//                        the work is cut into 64-row x K-split pieces that occupy every CU:
-//                        each workgroup stages its slice of A (all k rows) in LDS once, and
-//                        each of its 4 wavefronts streams 16 rows of W straight from HBM into
-//                        registers, all its K steps requested up front, into the 16x16x32
-//                        bf16 MFMA (W rows x prompts).  Float32 partial sums per K split.
-// decode_epilogue_kernel sums the K splits in a fixed order and applies the epilogue: the
-//                        residual add, SwiGLU over the interleaved gate/up rows, or RoPE at
-//                        the token's position with the query store and the key/value append.
+//                        the work is cut into about 1024 pieces of 64 rows x a K split:
+//                        each workgroup stages its slice of A (k rows, LDS sized to k) once,
+//                        and each of its 4 wavefronts streams 16 rows of W straight from HBM
+//                        into registers, all its K steps requested up front, into the
+//                        16x16x32 bf16 MFMA (W rows x prompts); float32 partial sums per
+//                        split.  The workgroup that completes a row group adds its splits in
+//                        a fixed order and applies the epilogue: the residual add, SwiGLU
+//                        over the interleaved gate/up rows, or RoPE at the token's position
+//                        with the query store and the key/value append.
 //
 // The chunks of the context part are counted from the prompt's first key, and the
 // generated keys form chunks of their own, so the packed and the full-batching layouts give
@@ -39,16 +40,20 @@
 
 namespace {
 
-constexpr int CH = ppk::kDecodeChunk;   // keys per chunk: 4 wavefronts x 8 iterations x 8 keys
+constexpr int CH = ppk::kDecodeChunk;   // keys per chunk: 4 wavefronts x IT iterations x 8 keys
+constexpr int IT = CH / 32;
 constexpr float kLog2e = 1.4426950408889634f;
 
 __global__ __launch_bounds__(64) void decode_prep_kernel(int k, int step, const int32_t* __restrict__ pos0,
                                                          const int32_t* __restrict__ gen_off, int D, double theta,
                                                          float2* __restrict__ table, int32_t* __restrict__ slot_pos,
                                                          int32_t* __restrict__ slot_kv, int32_t* __restrict__ slot_seg,
-                                                         int32_t* __restrict__ ident) {
+                                                         int32_t* __restrict__ ident, int32_t* __restrict__ counters,
+                                                         int n_counters) {
     const int i = blockIdx.x, j = threadIdx.x;
     if (i >= k) return;
+    if (i == 0)
+        for (int c = j; c < n_counters; c += 64) counters[c] = 0;
     const int half = D / 2;
     if (j < half) {
         const double inv_freq = pow(theta, -2.0 * j / static_cast<double>(D));
@@ -70,6 +75,26 @@ __device__ __forceinline__ void load_slice(const T* p, float* v) {
     for (int e = 0; e < DL; e += 8) load8(p + e, v + e);
 }
 
+// A slice of DL elements held as 16-byte pieces -> float.
+template <typename T, int DL>
+__device__ __forceinline__ void unpack_slice(const u32x4* raw, float* v) {
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int c = 0; c < DL / 8; ++c) {
+            const bf16x8 b = __builtin_bit_cast(bf16x8, raw[c]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[8 * c + e] = static_cast<float>(b[e]);
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < DL / 4; ++c) {
+            const f32x4 f = __builtin_bit_cast(f32x4, raw[c]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[4 * c + e] = f[e];
+        }
+    }
+}
+
 // (m, l, o) <- merge of two partial softmax results over disjoint key sets (base-2 scores).
 template <int DL>
 __device__ __forceinline__ void merge(float& m, float& l, float* o, float m2, float l2, const float* o2) {
@@ -83,7 +108,7 @@ __device__ __forceinline__ void merge(float& m, float& l, float* o, float m2, fl
 }
 
 // Lane l of wavefront w: key group kg = l / 8 (one key per iteration), dimension slice
-// dl = l % 8 (D / 8 consecutive elements).  Keys of the chunk: j0 + 64 w + 8 it + kg.
+// dl = l % 8 (D / 8 consecutive elements).  Keys of the chunk: j0 + 8 IT w + 8 it + kg.
 template <typename T, int D, int R>
 __global__ __launch_bounds__(256) void decode_attn_kernel(
     const T* __restrict__ q, int64_t ldq, const T* __restrict__ ctx_k, const T* __restrict__ ctx_v,
@@ -136,20 +161,32 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
         for (int e = 0; e < DL; ++e) o[r][e] = 0.f;
     }
     const int64_t col = int64_t(g) * D + dl * DL;
-#pragma unroll 2
-    for (int it = 0; it < 8; ++it) {
-        const int j = j0 + 64 * w + 8 * it + kg;
-        const bool in = j < jend;
-        float kf[DL], vf[DL];
-        if (in) {
-            const int64_t off = (row0 + j) * ldkv + col;
-            load_slice<T, DL>(K + off, kf);
-            load_slice<T, DL>(V + off, vf);
-        } else {
+    // every key and value slice of the chunk requested before the first score (rows past
+    // the chunk read as its last row, then ignored), so the HBM latency is paid once
+    constexpr int NQ = DL * int(sizeof(T)) / 16;      // 16-byte pieces per slice
+    u32x4 kraw[IT][NQ], vraw[IT][NQ];
 #pragma unroll
-            for (int e = 0; e < DL; ++e) kf[e] = vf[e] = 0.f;
+    for (int it = 0; it < IT; ++it) {
+        const int j = min(j0 + 8 * IT * w + 8 * it + kg, jend - 1);
+        const int64_t off = (row0 + j) * ldkv + col;
+#pragma unroll
+        for (int c = 0; c < NQ; ++c) {
+            kraw[it][c] = *reinterpret_cast<const u32x4*>(K + off + c * (16 / int(sizeof(T))));
+            vraw[it][c] = *reinterpret_cast<const u32x4*>(V + off + c * (16 / int(sizeof(T))));
         }
-        const bool ok = in && j < valid;  // padding of the full-batching layout is read, then masked
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+#pragma unroll
+        for (int c = 0; c < NQ; ++c) asm volatile("" : "+v"(kraw[it][c]), "+v"(vraw[it][c]));
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        const int j = j0 + 8 * IT * w + 8 * it + kg;
+        float kf[DL], vf[DL];
+        unpack_slice<T, DL>(kraw[it], kf);
+        unpack_slice<T, DL>(vraw[it], vf);
+        const bool ok = j < jend && j < valid;   // padding of the full-batching layout is read, then masked
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             float s = 0.f;
@@ -246,56 +283,13 @@ __device__ __forceinline__ int gsw(int r) { return (r & 1) | (((r >> 1) & 1) << 
 
 constexpr int SG_ROWS = 64;     // W rows per workgroup, 16 per wavefront
 constexpr int SG_TILE = 128;    // K columns per staged A tile
-constexpr int SG_MAX_TILES = 4; // A tiles per K split (64 KB of LDS at 64 prompts)
+constexpr int SG_MAX_TILES = 4; // A tiles per K split
 
-// part[s][m][n] = sum over the K tiles of split s of A[m, :] . W[n, :], for m < k <= 64.
-// Wavefront w owns W rows n0 = 64 blockIdx.x + 16 w .. + 15; lane l reads 8 consecutive K
-// values of row n0 + l % 16 at offset 8 (l / 16) of each 32-wide step, and holds, per prompt
-// block mb, the sums of prompt 16 mb + l % 16 for rows n0 + 4 (l / 16) + 0..3.
-__global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
-                                                          const bf16* __restrict__ W, int64_t ldw, int N, int K,
-                                                          int tiles_per_split, float* __restrict__ part) {
-    __shared__ __attribute__((aligned(16))) char lds[SG_MAX_TILES][64 * 256];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int lr = lane & 15, q4 = lane >> 4;
-    const int s = blockIdx.y;
-    const int t0 = s * tiles_per_split, nt = min(tiles_per_split, K / SG_TILE - t0);
-    const int nmb = (k + 15) / 16, k_pad = 16 * nmb;
-    // stage A[0 .. k_pad) x tiles t0 .. t0 + nt (rows past k read as row k - 1, never stored)
-    for (int idx = threadIdx.x; idx < k_pad * nt * 16; idx += 256) {
-        const int r = idx / (nt * 16), q = idx % (nt * 16), t = q / 16, ch = q % 16;
-        const bf16x8 v = *reinterpret_cast<const bf16x8*>(A + int64_t(min(r, k - 1)) * lda +
-                                                          int64_t(t0 + t) * SG_TILE + ch * 8);
-        *reinterpret_cast<bf16x8*>(lds[t] + r * 256 + 16 * (ch ^ gsw(r & 7))) = v;
-    }
-    const int n0 = blockIdx.x * SG_ROWS + 16 * w;
-    const bf16* wrow = W + int64_t(n0 + lr) * ldw + int64_t(t0) * SG_TILE + 8 * q4;
-    const int steps = 4 * nt;
-    bf16x8 ring[4 * SG_MAX_TILES];
-#pragma unroll
-    for (int j = 0; j < 4 * SG_MAX_TILES; ++j)
-        if (j < steps) ring[j] = *reinterpret_cast<const bf16x8*>(wrow + 32 * j);
-    __syncthreads();
-    f32x4 acc[4] = {};
-    const int fsw = gsw(lr & 7);
-#pragma unroll
-    for (int j = 0; j < 4 * SG_MAX_TILES; ++j) {
-        if (j >= steps) break;
-        const char* tile = lds[j / 4];
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-            if (mb >= nmb) break;
-            const bf16x8 h = *reinterpret_cast<const bf16x8*>(tile + (16 * mb + lr) * 256 +
-                                                              16 * ((4 * (j % 4) + q4) ^ fsw));
-            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[j], h, acc[mb], 0, 0, 0);
-        }
-    }
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-        const int m = 16 * mb + lr;
-        if (mb < nmb && m < k)
-            *reinterpret_cast<f32x4*>(part + (int64_t(s) * k + m) * N + n0 + 4 * q4) = acc[mb];
-    }
+// Row of W that lane row `lr` of wavefront w of row group g covers.  For the QKV projection
+// a row group takes 32 rows of a head's first half and their 32 rotate-half partners
+// (head dim 128: rows c and c + 64), so that RoPE needs no other workgroup.
+__device__ __forceinline__ int sg_row(bool pairs, int g, int w) {
+    return pairs ? (g >> 1) * 128 + (w >> 1) * 64 + (g & 1) * 32 + (w & 1) * 16 : g * SG_ROWS + 16 * w;
 }
 
 // Sum of the K splits of part at (m, n .. n + 3), in split order.
@@ -305,7 +299,129 @@ __device__ __forceinline__ f32x4 split_sum(const float* part, int S, int k, int 
     return v;
 }
 
-// One thread per 4 consecutive outputs of one prompt row.
+// part[s][m][n] = sum over the NT K tiles of split s of A[m, :] . W[n, :], m < k <= 16 NMB.
+// Lane l of wavefront w reads 8 consecutive K values of W row n_w + l % 16 at offset
+// 8 (l / 16) of each 32-wide step, every step of its split requested before the first MFMA,
+// and holds, per prompt block mb, the sums of prompt 16 mb + l % 16 for rows
+// n_w + 4 (l / 16) + 0..3.  The slice of A (k_pad rows x NT tiles) is staged once in LDS.
+// The workgroup that finishes a row group's last split (an atomic count per row group, reset
+// by that workgroup) adds the splits in split order and applies the epilogue, so the result
+// does not depend on which split finished last.
+template <int EPI, int NT, int NMB, bool FUSED>
+__global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
+                                                          const bf16* __restrict__ W, int64_t ldw, int N, int K,
+                                                          int splits, float* __restrict__ part,
+                                                          int32_t* __restrict__ counters, ppk::DecodeEpi ep) {
+    extern __shared__ __attribute__((aligned(16))) char lds[];   // NT tiles of 16 NMB rows x 256 bytes
+    __shared__ int last;
+    constexpr int KP = 16 * NMB, TILE_B = KP * 256;
+    constexpr bool PAIRS = EPI == ppk::kQkvRope;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lr = lane & 15, q4 = lane >> 4;
+    const int g = blockIdx.x, s = blockIdx.y;
+    const int t0 = s * NT;
+    const int nt = min(NT, K / SG_TILE - t0);     // the last split may hold fewer tiles
+    const int n_w = sg_row(PAIRS, g, w);
+    const bf16* wrow = W + int64_t(n_w + lr) * ldw + int64_t(t0) * SG_TILE + 8 * q4;
+    bf16x8 ring[4 * NT];
+#pragma unroll
+    for (int j = 0; j < 4 * NT; ++j)
+        if (j < 4 * nt) ring[j] = *reinterpret_cast<const bf16x8*>(wrow + 32 * j);
+    // stage A[0 .. KP) x tiles t0 .. t0 + nt (rows past k read as row k - 1, never stored)
+    for (int idx = threadIdx.x; idx < KP * nt * 16; idx += 256) {
+        const int r = idx / (nt * 16), q = idx % (nt * 16), t = q / 16, ch = q % 16;
+        const bf16x8 v = *reinterpret_cast<const bf16x8*>(A + int64_t(min(r, k - 1)) * lda +
+                                                          int64_t(t0 + t) * SG_TILE + ch * 8);
+        *reinterpret_cast<bf16x8*>(lds + t * TILE_B + r * 256 + 16 * (ch ^ gsw(r & 7))) = v;
+    }
+    // keep every W fragment in flight from the top: the compiler would otherwise sink each
+    // load to its MFMA and pay the HBM latency once per step
+#pragma unroll
+    for (int j = 0; j < 4 * NT; ++j) asm volatile("" : "+v"(ring[j]));
+    __syncthreads();
+    f32x4 acc[NMB] = {};
+    const int fsw = gsw(lr & 7);
+#pragma unroll
+    for (int j = 0; j < 4 * NT; ++j) {
+        if (j < 4 * nt) {
+#pragma unroll
+            for (int mb = 0; mb < NMB; ++mb) {
+                const bf16x8 h = *reinterpret_cast<const bf16x8*>(lds + (j / 4) * TILE_B + (16 * mb + lr) * 256 +
+                                                                  16 * ((4 * (j % 4) + q4) ^ fsw));
+                acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[j], h, acc[mb], 0, 0, 0);
+            }
+        }
+    }
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+        const int m = 16 * mb + lr;
+        if (m < k) *reinterpret_cast<f32x4*>(part + (int64_t(s) * k + m) * N + n_w + 4 * q4) = acc[mb];
+    }
+    if (!FUSED) return;
+    // the last workgroup of the row group finishes it
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) last = atomicAdd(&counters[g], 1) == splits - 1;
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    if (threadIdx.x == 0) counters[g] = 0;        // ready for the next launch
+    if (EPI == ppk::kResidual) {                  // x[m][n] += sum, the group's 64 rows
+        for (int it = threadIdx.x; it < k * 16; it += 256) {
+            const int m = it / 16, n = g * SG_ROWS + 4 * (it % 16);
+            f32x4* x = reinterpret_cast<f32x4*>(static_cast<float*>(ep.out) + int64_t(m) * ep.ldo + n);
+            *x = *x + split_sum(part, splits, k, N, m, n);
+        }
+    } else if (EPI == ppk::kSwiGLU) {             // rows 32 j + 0..15 gate, + 16..31 up, of feature 16 j + ..
+        for (int it = threadIdx.x; it < k * 8; it += 256) {
+            const int m = it / 8, q = it % 8;
+            const int f = g * 32 + 4 * q;          // 32 features per row group
+            const int n = 32 * (f / 16) + f % 16;
+            const f32x4 gt = split_sum(part, splits, k, N, m, n), up = split_sum(part, splits, k, N, m, n + 16);
+            bf16x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(gt[e]) * up[e]);
+            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + f) = o;
+        }
+    } else {                                      // QKV: pairs (i, i + 64) of head g / 2, i in 32 (g % 2) + ..
+        const ppk::QkvOut& qo = ep.qkv;
+        const int head = g >> 1;
+        const bool rotate = head < qo.H + qo.Hkv;
+        for (int it = threadIdx.x; it < k * 8; it += 256) {
+            const int m = it / 8, i = (g & 1) * 32 + 4 * (it % 8);
+            const int n = head * 128 + i;
+            const f32x4 a = split_sum(part, splits, k, N, m, n), b = split_sum(part, splits, k, N, m, n + 64);
+            bf16x4 lo, hi;
+            if (rotate) {
+                const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float2 t = cs[e];
+                    lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
+                    hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    lo[e] = static_cast<bf16>(a[e]);
+                    hi[e] = static_cast<bf16>(b[e]);
+                }
+            }
+            bf16* dst;
+            if (head < qo.H) {
+                dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
+            } else {
+                const bool key = rotate;
+                dst = static_cast<bf16*>(key ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
+                      (head - qo.H - (key ? 0 : qo.Hkv)) * 128;
+            }
+            *reinterpret_cast<bf16x4*>(dst + i) = lo;
+            *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+        }
+    }
+}
+
+// The split sums and the epilogue as a kernel of their own, one thread per 4 outputs.
 template <int EPI>
 __global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __restrict__ part, int S, int k, int N,
                                                               ppk::DecodeEpi ep) {
@@ -328,14 +444,15 @@ __global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __res
         *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + f) = o;
     } else {                               // QKV: RoPE on q and k (pairs i, i + 64), store / append
         const ppk::QkvOut& qo = ep.qkv;
-        const int heads = qo.H + 2 * qo.Hkv, per = heads * 16;   // 16 quads per head of 128
+        const int heads = qo.H + 2 * qo.Hkv, per = heads * 16;   // 16 pairs of quads per head of 128
         if (idx >= int64_t(k) * per) return;
         const int m = static_cast<int>(idx / per), r = static_cast<int>(idx % per);
         const int head = r / 16, i = (r % 16) * 4;
         const int n = head * 128 + i;
         const f32x4 a = split_sum(part, S, k, N, m, n), b = split_sum(part, S, k, N, m, n + 64);
         bf16x4 lo, hi;
-        if (head < qo.H + qo.Hkv) {
+        const bool rotate = head < qo.H + qo.Hkv;
+        if (rotate) {
             const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -354,12 +471,87 @@ __global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __res
         if (head < qo.H) {
             dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
         } else {
-            const bool key = head < qo.H + qo.Hkv;
-            dst = static_cast<bf16*>(key ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
-                  (head - qo.H - (key ? 0 : qo.Hkv)) * 128;
+            dst = static_cast<bf16*>(rotate ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
+                  (head - qo.H - (rotate ? 0 : qo.Hkv)) * 128;
         }
         *reinterpret_cast<bf16x4*>(dst + i) = lo;
         *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+    }
+}
+
+constexpr bool kFusedTail = false;   // epilogue in the GEMM's last workgroup (true) or its own kernel
+
+// Residual add of a split-K projection fused with the RMSNorm that follows it, one workgroup
+// of d / 4 threads per prompt row, 4 consecutive elements per thread: x[m] += sum over splits
+// of part[.][m] (split order; all S loads of a thread issued together), stored back; then
+// out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * g.  S = 0: no pending projection.
+template <typename TO>
+__global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ part,
+                                                                int S, int k, int d, const float* __restrict__ g,
+                                                                TO* __restrict__ out, float eps) {
+    __shared__ float red[16];
+    const int m = blockIdx.x, c = 4 * threadIdx.x;
+    float* xr = x + int64_t(m) * d + c;
+    f32x4 v = *reinterpret_cast<const f32x4*>(xr);
+    if (S > 0) {
+        const float* p = part + int64_t(m) * d + c;
+        const int64_t stride = int64_t(k) * d;
+        int s = 0;
+        for (; s + 4 <= S; s += 4) {
+            const f32x4 a0 = *reinterpret_cast<const f32x4*>(p + s * stride);
+            const f32x4 a1 = *reinterpret_cast<const f32x4*>(p + (s + 1) * stride);
+            const f32x4 a2 = *reinterpret_cast<const f32x4*>(p + (s + 2) * stride);
+            const f32x4 a3 = *reinterpret_cast<const f32x4*>(p + (s + 3) * stride);
+            v += a0;
+            v += a1;
+            v += a2;
+            v += a3;
+        }
+        for (; s < S; ++s) v += *reinterpret_cast<const f32x4*>(p + s * stride);
+        *reinterpret_cast<f32x4*>(xr) = v;
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ss = fmaf(v[e], v[e], ss);
+    ss = wave_sum(ss);
+    const int nw = blockDim.x / 64;
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    float tot = 0.f;
+    for (int i = 0; i < nw; ++i) tot += red[i];
+    const float r = rsqrtf(tot / static_cast<float>(d) + eps);
+    const f32x4 gg = *reinterpret_cast<const f32x4*>(g + c);
+    if constexpr (sizeof(TO) == 2) {
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(v[e] * r * gg[e]);
+        *reinterpret_cast<bf16x4*>(out + int64_t(m) * d + c) = o;
+    } else {
+        *reinterpret_cast<f32x4*>(out + int64_t(m) * d + c) = v * r * gg;
+    }
+}
+
+template <int EPI, int NT>
+void launch_skinny_nt(int nmb, dim3 grid, size_t lds, hipStream_t s, const bf16* A, int64_t lda, int k,
+                      const bf16* W, int64_t ldw, int N, int K, int splits, float* part, int32_t* counters,
+                      const ppk::DecodeEpi& ep) {
+    switch (nmb) {
+        case 1: skinny_gemm_kernel<EPI, NT, 1, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        case 2: skinny_gemm_kernel<EPI, NT, 2, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        case 3: skinny_gemm_kernel<EPI, NT, 3, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        default: skinny_gemm_kernel<EPI, NT, 4, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+    }
+}
+
+template <int EPI>
+void launch_skinny(int nt, int nmb, dim3 grid, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W,
+                   int64_t ldw, int N, int K, int splits, float* part, int32_t* counters, const ppk::DecodeEpi& ep) {
+    const size_t lds = size_t(nt) * 16 * nmb * 256;
+    switch (nt) {
+        case 1: launch_skinny_nt<EPI, 1>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        case 2: launch_skinny_nt<EPI, 2>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        case 3: launch_skinny_nt<EPI, 3>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        default: launch_skinny_nt<EPI, 4>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
     }
 }
 
@@ -409,9 +601,10 @@ void attn_dispatch(int D, int R, const void* q, int64_t ldq, const void* ctx_k, 
 namespace ppk {
 
 void decode_prep(const DecodeLayout& Ly, int step, int D, float theta, float2* table, int32_t* slot_pos,
-                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, hipStream_t s) {
+                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, int32_t* counters, int n_counters,
+                 hipStream_t s) {
     decode_prep_kernel<<<Ly.k, 64, 0, s>>>(Ly.k, step, Ly.pos0, Ly.gen_off, D, static_cast<double>(theta), table,
-                                           slot_pos, slot_kv, slot_seg, ident);
+                                           slot_pos, slot_kv, slot_seg, ident, counters, n_counters);
 }
 
 void decode_attention(int dtype, const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v,
@@ -426,23 +619,39 @@ void decode_attention(int dtype, const void* q, int64_t ldq, const void* ctx_k, 
 
 SkinnySplit skinny_split(int N, int K) {
     const int tiles = K / SG_TILE, groups = N / SG_ROWS;
-    const int target = std::max(1, (512 + groups - 1) / groups);   // about 512 workgroups
+    const int target = std::max(1, (1024 + groups - 1) / groups);   // about 1024 workgroups
     const int per = std::min(SG_MAX_TILES, std::max(1, (tiles + target - 1) / target));
     return SkinnySplit{per, (tiles + per - 1) / per};
 }
 
 bool skinny_ok(int k, int N, int K) { return k >= 1 && k <= 64 && N % SG_ROWS == 0 && K % SG_TILE == 0; }
 
+int skinny_counters(int N) { return N / SG_ROWS; }
+
+void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
+                      float eps, hipStream_t s) {
+    const int threads = d / 4;   // d % 256 == 0 and d <= 4096: whole wavefronts, at most 1024 threads
+    if (dtype_out == PP_BF16)
+        residual_rmsnorm_kernel<bf16><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<bf16*>(out), eps);
+    else
+        residual_rmsnorm_kernel<float><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<float*>(out), eps);
+}
+
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
-                 const DecodeEpi& ep, hipStream_t s) {
+                 int32_t* counters, const DecodeEpi& ep, hipStream_t s) {
     const SkinnySplit sp = skinny_split(N, K);
-    skinny_gemm_kernel<<<dim3(N / SG_ROWS, sp.splits), 256, 0, s>>>(static_cast<const bf16*>(A), lda, k,
-                                                                      static_cast<const bf16*>(W), ldw, N, K,
-                                                                      sp.tiles_per_split, part);
-    int64_t threads;
-    if (epi == kResidual) threads = int64_t(k) * (N / 4);
-    else if (epi == kSwiGLU) threads = int64_t(k) * (N / 8);
-    else threads = int64_t(k) * (N / 128) * 16;           // (H + 2 Hkv) heads x 16 pairs of quads
+    const dim3 grid(N / SG_ROWS, sp.splits);
+    const int nmb = (k + 15) / 16;
+    const bf16* a = static_cast<const bf16*>(A);
+    const bf16* w = static_cast<const bf16*>(W);
+    if (epi == kResidual)
+        launch_skinny<kResidual>(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, sp.splits, part, counters, ep);
+    else if (epi == kSwiGLU)
+        launch_skinny<kSwiGLU>(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, sp.splits, part, counters, ep);
+    else
+        launch_skinny<kQkvRope>(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, sp.splits, part, counters, ep);
+    if (kFusedTail || epi == kResidual) return;   // residual: added by residual_rmsnorm
+    const int64_t threads = int64_t(k) * (epi == kResidual ? N / 4 : N / 8);
     const int blocks = static_cast<int>((threads + 255) / 256);
     if (epi == kResidual)
         decode_epilogue_kernel<kResidual><<<blocks, 256, 0, s>>>(part, sp.splits, k, N, ep);

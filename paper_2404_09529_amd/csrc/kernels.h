@@ -93,7 +93,7 @@ void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, i
                  int d, void* workspace, float* logits, int32_t* tokens, hipStream_t s);
 
 // ---------------------------------------------------------------------- generation (decode)
-constexpr int kDecodeChunk = 256;   // keys per workgroup of the decode attention
+constexpr int kDecodeChunk = 128;   // keys per workgroup of the decode attention
 
 // Device view of a generation layout (pp_gen_dlayout) with the chunk counts of its keys:
 // n_ctx_chunks = ceil(max_len / kDecodeChunk), n_gen_chunks = ceil(n_new / kDecodeChunk).
@@ -104,9 +104,10 @@ struct DecodeLayout {
 
 // Per prompt i < k for decode step `step`: table[i] = cos/sin((pos0[i] + step) theta^(-2j/D))
 // for j < D/2 (float64, float2 [k][D/2]); slot_pos[i] = i; slot_kv[i] = gen_off[i] + step;
-// slot_seg[i] = 0; ident[i] = i for i <= k (k + 1 entries).
+// slot_seg[i] = 0; ident[i] = i for i <= k (k + 1 entries); counters[0 .. n_counters) = 0.
 void decode_prep(const DecodeLayout& Ly, int step, int D, float theta, float2* table, int32_t* slot_pos,
-                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, hipStream_t s);
+                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, int32_t* counters, int n_counters,
+                 hipStream_t s);
 
 // One query row per prompt (q [k, ldq], H heads of D) against the prompt's context rows
 // ctx_off[i] .. + ctx_span[i] of ctx_k / ctx_v (rows past ctx_valid[i] masked) and its
@@ -134,9 +135,19 @@ SkinnySplit skinny_split(int N, int K);
 // Shapes the skinny GEMM takes: 1 <= k <= 64 rows, N % 64 == 0, K % 128 == 0.
 bool skinny_ok(int k, int N, int K);
 
+// Row-group completion counters decode_gemm needs for N output rows (int32 each); they must
+// be zero before the first call and are zero again after every call.
+int skinny_counters(int N);
+
+// x[m] += sum of the S splits of part (split order; S = 0: nothing), stored back, then
+// out[m] = RMSNorm(x[m]) * g in dtype_out (PP_BF16 or PP_F32); k rows of d <= 4096.
+void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
+                      float eps, hipStream_t s);
+
 // bf16 C = A W^T for k <= 64 rows (A [k, lda], W [N, ldw]) through float32 partial sums
-// (part: splits * k * N floats) and the epilogue `epi` (kResidual, kSwiGLU or kQkvRope).
+// (part: splits * k * N floats) and the epilogue `epi`: kSwiGLU or kQkvRope are applied by
+// a second kernel; kResidual leaves the partial sums for residual_rmsnorm to add.
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
-                 const DecodeEpi& ep, hipStream_t s);
+                 int32_t* counters, const DecodeEpi& ep, hipStream_t s);
 
 }  // namespace ppk

@@ -121,3 +121,9 @@ def test_dataset_packing_rebuilds_the_oracle_rows(name, bs):
             segs = plan.seg_prompt[plan.row_seg_ptr[r]:plan.row_seg_ptr[r + 1]]
             got.append(sorted(int(ids[s]) for s in segs))
         assert sorted(got) == sorted(want)
+
+
+def test_linear_fit_of_a_constant_predictor_is_none():
+    # batch size 1: every batch has r/k = 1
+    assert bench.linear_fit([1.0, 1.0, 1.0], [0.99, 1.0, 1.01]) is None
+    assert bench.linear_fit([0.5, 0.6, 0.7], [1.0, 1.0, 1.0]) is None
