@@ -32,8 +32,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 size_t elem_size(int dtype) { return dtype == PP_BF16 ? 2 : 4; }
 
 struct Layout {
-    size_t x = 0, xn = 0, q = 0, attn = 0, act = 0, gu = 0, h = 0, part = 0, table = 0, ints = 0, counters = 0,
-           ft = 0, gpart = 0, total = 0;
+    size_t x = 0, xn = 0, q = 0, attn = 0, act = 0, gu = 0, h = 0, part = 0, table = 0, ints = 0, ft = 0, gpart = 0,
+           total = 0;
 };
 
 // The projections of a decode step as (N, K).
@@ -60,15 +60,6 @@ bool use_skinny(const pp_config* c, int k) {
 
 int chunks(int n) { return (n + ppk::kDecodeChunk - 1) / ppk::kDecodeChunk; }
 
-// Row-group counters of the split-K projections (one array, reused by every projection).
-int n_counters(const pp_config* c) {
-    Proj p[4];
-    projections(c, p);
-    int n = 0;
-    for (const Proj& q : p) n = std::max(n, q.N % 64 == 0 ? ppk::skinny_counters(q.N) : 0);
-    return n;
-}
-
 Layout layout_of(const pp_config* c, const pp_gen_dlayout* g) {
     const size_t k = g->k, e = elem_size(c->dtype);
     const size_t d = c->d_model, F = c->ffn_dim, D = c->head_dim;
@@ -91,7 +82,6 @@ Layout layout_of(const pp_config* c, const pp_gen_dlayout* g) {
     L.part = take(k * size_t(c->n_heads) * nch * (D + 4) * 4);
     L.table = take(k * (D / 2) * sizeof(float2));
     L.ints = take((4 * k + 1) * sizeof(int32_t));
-    L.counters = take(size_t(n_counters(c)) * sizeof(int32_t));
     L.ft = take(ppk::first_token_workspace(c->dtype, g->k, c->vocab, c->d_model));
     size_t gpart = 0;
     if (use_skinny(c, g->k)) {
@@ -168,8 +158,6 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
     int32_t* slot_kv = slot_pos + k;
     int32_t* slot_seg = slot_kv + k;
     int32_t* ident = slot_seg + k;        // k + 1 entries
-    int32_t* counters = reinterpret_cast<int32_t*>(ws + L.counters);
-    const int nc = n_counters(cfg);
     const size_t ctx_layer = size_t(g->ctx_rows) * kvw * e, gen_layer = size_t(g->gen_rows) * kvw * e;
     const ppk::DecodeLayout Ly{k, chunks(g->max_len), chunks(g->n_new), g->ctx_off, g->ctx_span, g->ctx_valid,
                                g->pos0, g->gen_off};
@@ -186,7 +174,7 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
             ppk::rmsnorm(out_dtype, x, gain, out, k, d, eps, s);
         pending = 0;
     };
-    ppk::decode_prep(Ly, step, D, cfg->rope_theta, table, slot_pos, slot_kv, slot_seg, ident, counters, nc, s);
+    ppk::decode_prep(Ly, step, D, cfg->rope_theta, table, slot_pos, slot_kv, slot_seg, ident, s);
     ppk::embed(dt, x, w->embed, cfg->vocab, tokens_in, ident, k, d, s);
     for (int l = 0; l < cfg->n_layers; ++l) {
         const void* ck = static_cast<const char*>(ctx_k) + l * ctx_layer;
@@ -196,10 +184,10 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
         norm(w->attn_norm[l], xn, dt);
         if (skinny) {
             const ppk::QkvOut qo{q, hd, gk, gv, kvw, table, slot_pos, slot_kv, H, Hkv};
-            ppk::decode_gemm(ppk::kQkvRope, xn, d, k, w->wqkv[l], d, qkv_w, d, gpart, counters,
+            ppk::decode_gemm(ppk::kQkvRope, xn, d, k, w->wqkv[l], d, qkv_w, d, gpart,
                              ppk::DecodeEpi{nullptr, 0, qo}, s);
             ppk::decode_attention(dt, q, hd, ck, cv, gk, gv, kvw, Ly, step, H, Hkv, D, part, attn, hd, s);
-            ppk::decode_gemm(ppk::kResidual, attn, hd, k, w->wo[l], hd, d, hd, gpart, counters, ppk::DecodeEpi{x, d, qo},
+            ppk::decode_gemm(ppk::kResidual, attn, hd, k, w->wo[l], hd, d, hd, gpart, ppk::DecodeEpi{x, d, qo},
                              s);
             pending = ppk::skinny_split(d, hd).splits;
         } else if (bf) {
@@ -220,9 +208,9 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
         norm(w->mlp_norm[l], xn, dt);
         if (skinny) {
             const ppk::QkvOut none{};
-            ppk::decode_gemm(ppk::kSwiGLU, xn, d, k, w->w_gateup[l], d, 2 * F, d, gpart, counters,
+            ppk::decode_gemm(ppk::kSwiGLU, xn, d, k, w->w_gateup[l], d, 2 * F, d, gpart,
                              ppk::DecodeEpi{act, F, none}, s);
-            ppk::decode_gemm(ppk::kResidual, act, F, k, w->w_down[l], F, d, F, gpart, counters,
+            ppk::decode_gemm(ppk::kResidual, act, F, k, w->w_down[l], F, d, F, gpart,
                              ppk::DecodeEpi{x, d, none}, s);
             pending = ppk::skinny_split(d, F).splits;
         } else if (bf) {

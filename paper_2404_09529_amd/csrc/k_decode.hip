@@ -1,7 +1,7 @@
 // Generation with packed KV caches (section 4.8): the kernels of one decode step that the
 // prefill does not already have.  Each step feeds one new token per prompt through the
 // decoder (section 2.2: one forward pass per token, earlier keys and values read from the
-// cache); the projections reuse the prefill's GEMMs with one row per prompt.
+// cache).
 //
 // decode_prep_kernel     per prompt: the token's position pos0 + step (restart positions,
 //                        section 3.2, continued into generation), cos/sin of that position
@@ -21,10 +21,13 @@
 //                        and each of its 4 wavefronts streams 16 rows of W straight from HBM
 //                        into registers, all its K steps requested up front, into the
 //                        16x16x32 bf16 MFMA (W rows x prompts); float32 partial sums per
-//                        split.  The workgroup that completes a row group adds its splits in
-//                        a fixed order and applies the epilogue: the residual add, SwiGLU
-//                        over the interleaved gate/up rows, or RoPE at the token's position
-//                        with the query store and the key/value append.
+//                        split, added in split order by the kernel that consumes them.
+// decode_epilogue_kernel SwiGLU over the interleaved gate/up rows, or RoPE at the token's
+//                        position with the query store and the key/value append.
+// residual_rmsnorm_kernel  the residual add of the O and down projections fused with the
+//                        RMSNorm that follows each.
+// (A single-kernel split-K with the sum done by the last workgroup of a row group was
+// measured slower: its cross-workgroup hand-off costs more than the launch it saves.)
 //
 // The chunks of the context part are counted from the prompt's first key, and the
 // generated keys form chunks of their own, so the packed and the full-batching layouts give
@@ -48,12 +51,9 @@ __global__ __launch_bounds__(64) void decode_prep_kernel(int k, int step, const 
                                                          const int32_t* __restrict__ gen_off, int D, double theta,
                                                          float2* __restrict__ table, int32_t* __restrict__ slot_pos,
                                                          int32_t* __restrict__ slot_kv, int32_t* __restrict__ slot_seg,
-                                                         int32_t* __restrict__ ident, int32_t* __restrict__ counters,
-                                                         int n_counters) {
+                                                         int32_t* __restrict__ ident) {
     const int i = blockIdx.x, j = threadIdx.x;
     if (i >= k) return;
-    if (i == 0)
-        for (int c = j; c < n_counters; c += 64) counters[c] = 0;
     const int half = D / 2;
     if (j < half) {
         const double inv_freq = pow(theta, -2.0 * j / static_cast<double>(D));
@@ -285,43 +285,23 @@ constexpr int SG_ROWS = 64;     // W rows per workgroup, 16 per wavefront
 constexpr int SG_TILE = 128;    // K columns per staged A tile
 constexpr int SG_MAX_TILES = 4; // A tiles per K split
 
-// Row of W that lane row `lr` of wavefront w of row group g covers.  For the QKV projection
-// a row group takes 32 rows of a head's first half and their 32 rotate-half partners
-// (head dim 128: rows c and c + 64), so that RoPE needs no other workgroup.
-__device__ __forceinline__ int sg_row(bool pairs, int g, int w) {
-    return pairs ? (g >> 1) * 128 + (w >> 1) * 64 + (g & 1) * 32 + (w & 1) * 16 : g * SG_ROWS + 16 * w;
-}
-
-// Sum of the K splits of part at (m, n .. n + 3), in split order.
-__device__ __forceinline__ f32x4 split_sum(const float* part, int S, int k, int N, int m, int n) {
-    f32x4 v = *reinterpret_cast<const f32x4*>(part + int64_t(m) * N + n);
-    for (int s = 1; s < S; ++s) v += *reinterpret_cast<const f32x4*>(part + (int64_t(s) * k + m) * N + n);
-    return v;
-}
-
 // part[s][m][n] = sum over the NT K tiles of split s of A[m, :] . W[n, :], m < k <= 16 NMB.
 // Lane l of wavefront w reads 8 consecutive K values of W row n_w + l % 16 at offset
 // 8 (l / 16) of each 32-wide step, every step of its split requested before the first MFMA,
 // and holds, per prompt block mb, the sums of prompt 16 mb + l % 16 for rows
 // n_w + 4 (l / 16) + 0..3.  The slice of A (k_pad rows x NT tiles) is staged once in LDS.
-// The workgroup that finishes a row group's last split (an atomic count per row group, reset
-// by that workgroup) adds the splits in split order and applies the epilogue, so the result
-// does not depend on which split finished last.
-template <int EPI, int NT, int NMB, bool FUSED>
+template <int NT, int NMB>
 __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
                                                           const bf16* __restrict__ W, int64_t ldw, int N, int K,
-                                                          int splits, float* __restrict__ part,
-                                                          int32_t* __restrict__ counters, ppk::DecodeEpi ep) {
+                                                          float* __restrict__ part) {
     extern __shared__ __attribute__((aligned(16))) char lds[];   // NT tiles of 16 NMB rows x 256 bytes
-    __shared__ int last;
     constexpr int KP = 16 * NMB, TILE_B = KP * 256;
-    constexpr bool PAIRS = EPI == ppk::kQkvRope;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int lr = lane & 15, q4 = lane >> 4;
-    const int g = blockIdx.x, s = blockIdx.y;
+    const int g = blockIdx.x, s = blockIdx.y;   // row group, K split
     const int t0 = s * NT;
     const int nt = min(NT, K / SG_TILE - t0);     // the last split may hold fewer tiles
-    const int n_w = sg_row(PAIRS, g, w);
+    const int n_w = g * SG_ROWS + 16 * w;
     const bf16* wrow = W + int64_t(n_w + lr) * ldw + int64_t(t0) * SG_TILE + 8 * q4;
     bf16x8 ring[4 * NT];
 #pragma unroll
@@ -357,68 +337,13 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
         const int m = 16 * mb + lr;
         if (m < k) *reinterpret_cast<f32x4*>(part + (int64_t(s) * k + m) * N + n_w + 4 * q4) = acc[mb];
     }
-    if (!FUSED) return;
-    // the last workgroup of the row group finishes it
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) last = atomicAdd(&counters[g], 1) == splits - 1;
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
-    if (threadIdx.x == 0) counters[g] = 0;        // ready for the next launch
-    if (EPI == ppk::kResidual) {                  // x[m][n] += sum, the group's 64 rows
-        for (int it = threadIdx.x; it < k * 16; it += 256) {
-            const int m = it / 16, n = g * SG_ROWS + 4 * (it % 16);
-            f32x4* x = reinterpret_cast<f32x4*>(static_cast<float*>(ep.out) + int64_t(m) * ep.ldo + n);
-            *x = *x + split_sum(part, splits, k, N, m, n);
-        }
-    } else if (EPI == ppk::kSwiGLU) {             // rows 32 j + 0..15 gate, + 16..31 up, of feature 16 j + ..
-        for (int it = threadIdx.x; it < k * 8; it += 256) {
-            const int m = it / 8, q = it % 8;
-            const int f = g * 32 + 4 * q;          // 32 features per row group
-            const int n = 32 * (f / 16) + f % 16;
-            const f32x4 gt = split_sum(part, splits, k, N, m, n), up = split_sum(part, splits, k, N, m, n + 16);
-            bf16x4 o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(gt[e]) * up[e]);
-            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + f) = o;
-        }
-    } else {                                      // QKV: pairs (i, i + 64) of head g / 2, i in 32 (g % 2) + ..
-        const ppk::QkvOut& qo = ep.qkv;
-        const int head = g >> 1;
-        const bool rotate = head < qo.H + qo.Hkv;
-        for (int it = threadIdx.x; it < k * 8; it += 256) {
-            const int m = it / 8, i = (g & 1) * 32 + 4 * (it % 8);
-            const int n = head * 128 + i;
-            const f32x4 a = split_sum(part, splits, k, N, m, n), b = split_sum(part, splits, k, N, m, n + 64);
-            bf16x4 lo, hi;
-            if (rotate) {
-                const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float2 t = cs[e];
-                    lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
-                    hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    lo[e] = static_cast<bf16>(a[e]);
-                    hi[e] = static_cast<bf16>(b[e]);
-                }
-            }
-            bf16* dst;
-            if (head < qo.H) {
-                dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
-            } else {
-                const bool key = rotate;
-                dst = static_cast<bf16*>(key ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
-                      (head - qo.H - (key ? 0 : qo.Hkv)) * 128;
-            }
-            *reinterpret_cast<bf16x4*>(dst + i) = lo;
-            *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
-        }
-    }
+}
+
+// Sum of the K splits of part at (m, n .. n + 3), in split order.
+__device__ __forceinline__ f32x4 split_sum(const float* part, int S, int k, int N, int m, int n) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(part + int64_t(m) * N + n);
+    for (int s = 1; s < S; ++s) v += *reinterpret_cast<const f32x4*>(part + (int64_t(s) * k + m) * N + n);
+    return v;
 }
 
 // The split sums and the epilogue as a kernel of their own, one thread per 4 outputs.
@@ -479,7 +404,6 @@ __global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __res
     }
 }
 
-constexpr bool kFusedTail = false;   // epilogue in the GEMM's last workgroup (true) or its own kernel
 
 // Residual add of a split-K projection fused with the RMSNorm that follows it, one workgroup
 // of d / 4 threads per prompt row, 4 consecutive elements per thread: x[m] += sum over splits
@@ -531,27 +455,25 @@ __global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restric
     }
 }
 
-template <int EPI, int NT>
+template <int NT>
 void launch_skinny_nt(int nmb, dim3 grid, size_t lds, hipStream_t s, const bf16* A, int64_t lda, int k,
-                      const bf16* W, int64_t ldw, int N, int K, int splits, float* part, int32_t* counters,
-                      const ppk::DecodeEpi& ep) {
+                      const bf16* W, int64_t ldw, int N, int K, float* part) {
     switch (nmb) {
-        case 1: skinny_gemm_kernel<EPI, NT, 1, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
-        case 2: skinny_gemm_kernel<EPI, NT, 2, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
-        case 3: skinny_gemm_kernel<EPI, NT, 3, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
-        default: skinny_gemm_kernel<EPI, NT, 4, kFusedTail><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        case 1: skinny_gemm_kernel<NT, 1><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
+        case 2: skinny_gemm_kernel<NT, 2><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
+        case 3: skinny_gemm_kernel<NT, 3><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
+        default: skinny_gemm_kernel<NT, 4><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
     }
 }
 
-template <int EPI>
 void launch_skinny(int nt, int nmb, dim3 grid, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W,
-                   int64_t ldw, int N, int K, int splits, float* part, int32_t* counters, const ppk::DecodeEpi& ep) {
+                   int64_t ldw, int N, int K, float* part) {
     const size_t lds = size_t(nt) * 16 * nmb * 256;
     switch (nt) {
-        case 1: launch_skinny_nt<EPI, 1>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
-        case 2: launch_skinny_nt<EPI, 2>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
-        case 3: launch_skinny_nt<EPI, 3>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
-        default: launch_skinny_nt<EPI, 4>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, splits, part, counters, ep); break;
+        case 1: launch_skinny_nt<1>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
+        case 2: launch_skinny_nt<2>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
+        case 3: launch_skinny_nt<3>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
+        default: launch_skinny_nt<4>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
     }
 }
 
@@ -601,10 +523,9 @@ void attn_dispatch(int D, int R, const void* q, int64_t ldq, const void* ctx_k, 
 namespace ppk {
 
 void decode_prep(const DecodeLayout& Ly, int step, int D, float theta, float2* table, int32_t* slot_pos,
-                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, int32_t* counters, int n_counters,
-                 hipStream_t s) {
+                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, hipStream_t s) {
     decode_prep_kernel<<<Ly.k, 64, 0, s>>>(Ly.k, step, Ly.pos0, Ly.gen_off, D, static_cast<double>(theta), table,
-                                           slot_pos, slot_kv, slot_seg, ident, counters, n_counters);
+                                           slot_pos, slot_kv, slot_seg, ident);
 }
 
 void decode_attention(int dtype, const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v,
@@ -626,8 +547,6 @@ SkinnySplit skinny_split(int N, int K) {
 
 bool skinny_ok(int k, int N, int K) { return k >= 1 && k <= 64 && N % SG_ROWS == 0 && K % SG_TILE == 0; }
 
-int skinny_counters(int N) { return N / SG_ROWS; }
-
 void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
                       float eps, hipStream_t s) {
     const int threads = d / 4;   // d % 256 == 0 and d <= 4096: whole wavefronts, at most 1024 threads
@@ -638,19 +557,14 @@ void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, 
 }
 
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
-                 int32_t* counters, const DecodeEpi& ep, hipStream_t s) {
+                 const DecodeEpi& ep, hipStream_t s) {
     const SkinnySplit sp = skinny_split(N, K);
     const dim3 grid(N / SG_ROWS, sp.splits);
     const int nmb = (k + 15) / 16;
     const bf16* a = static_cast<const bf16*>(A);
     const bf16* w = static_cast<const bf16*>(W);
-    if (epi == kResidual)
-        launch_skinny<kResidual>(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, sp.splits, part, counters, ep);
-    else if (epi == kSwiGLU)
-        launch_skinny<kSwiGLU>(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, sp.splits, part, counters, ep);
-    else
-        launch_skinny<kQkvRope>(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, sp.splits, part, counters, ep);
-    if (kFusedTail || epi == kResidual) return;   // residual: added by residual_rmsnorm
+    launch_skinny(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, part);
+    if (epi == kResidual) return;   // the residual add happens in residual_rmsnorm
     const int64_t threads = int64_t(k) * (epi == kResidual ? N / 4 : N / 8);
     const int blocks = static_cast<int>((threads + 255) / 256);
     if (epi == kResidual)

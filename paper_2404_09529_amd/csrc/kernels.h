@@ -104,10 +104,9 @@ struct DecodeLayout {
 
 // Per prompt i < k for decode step `step`: table[i] = cos/sin((pos0[i] + step) theta^(-2j/D))
 // for j < D/2 (float64, float2 [k][D/2]); slot_pos[i] = i; slot_kv[i] = gen_off[i] + step;
-// slot_seg[i] = 0; ident[i] = i for i <= k (k + 1 entries); counters[0 .. n_counters) = 0.
+// slot_seg[i] = 0; ident[i] = i for i <= k (k + 1 entries).
 void decode_prep(const DecodeLayout& Ly, int step, int D, float theta, float2* table, int32_t* slot_pos,
-                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, int32_t* counters, int n_counters,
-                 hipStream_t s);
+                 int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, hipStream_t s);
 
 // One query row per prompt (q [k, ldq], H heads of D) against the prompt's context rows
 // ctx_off[i] .. + ctx_span[i] of ctx_k / ctx_v (rows past ctx_valid[i] masked) and its
@@ -135,10 +134,6 @@ SkinnySplit skinny_split(int N, int K);
 // Shapes the skinny GEMM takes: 1 <= k <= 64 rows, N % 64 == 0, K % 128 == 0.
 bool skinny_ok(int k, int N, int K);
 
-// Row-group completion counters decode_gemm needs for N output rows (int32 each); they must
-// be zero before the first call and are zero again after every call.
-int skinny_counters(int N);
-
 // x[m] += sum of the S splits of part (split order; S = 0: nothing), stored back, then
 // out[m] = RMSNorm(x[m]) * g in dtype_out (PP_BF16 or PP_F32); k rows of d <= 4096.
 void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
@@ -148,6 +143,6 @@ void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, 
 // (part: splits * k * N floats) and the epilogue `epi`: kSwiGLU or kQkvRope are applied by
 // a second kernel; kResidual leaves the partial sums for residual_rmsnorm to add.
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
-                 int32_t* counters, const DecodeEpi& ep, hipStream_t s);
+                 const DecodeEpi& ep, hipStream_t s);
 
 }  // namespace ppk

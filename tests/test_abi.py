@@ -330,9 +330,8 @@ def test_decode_workspace_and_rejections(L):
         return -(-tiles // per)
     proj = [(48 * 128, d), (d, H * D), (2 * F, d), (d, F)]
     gpart = max(splits(N, K) * k * N * 4 for N, K in proj)
-    counters = max(N // 64 for N, _ in proj) * 4
     want = (k * d * 4 + k * d * 2 + k * H * D * 2 + k * H * D * 2 + k * F * 2 + k * d * 4
-            + k * H * chunks * (D + 4) * 4 + k * 64 * 8 + (4 * k + 1) * 4 + counters + 16 * d * 2 + 250 * k * 8
+            + k * H * chunks * (D + 4) * 4 + k * 64 * 8 + (4 * k + 1) * 4 + 16 * d * 2 + 250 * k * 8
             + gpart)
     assert want <= n.value <= want + 14 * 256
     ws = n.value
