@@ -405,6 +405,124 @@ __global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __res
 }
 
 
+// Decode projections whose epilogue needs two blocks of 16 weight rows together, SwiGLU (the
+// 16 gate rows and the 16 up rows of 16 features) and QKV (16 rotate-half pairs c, c + 64 of
+// a head): one workgroup per such 32 rows, its 4 wavefronts each taking a quarter of K, the
+// quarters added in wavefront order through LDS and the epilogue applied in the same kernel
+// (no partial sums leave the workgroup).  Weight and activation fragments are read straight
+// from global memory into a ring of RP_RING steps.  Lane l: weight row r_nb + l % 16 and prompt 16 mb + l % 16, K offset
+// 8 (l / 16) of each 32-wide step; it ends with block nb's rows r_nb + 4 (l / 16) + 0..3 for
+// prompt 16 mb + l % 16.
+constexpr int RP_RING = 8;
+constexpr bool kRowPairs = true;   // SwiGLU and QKV projections: paired rows (true) or split-K + epilogue kernel
+
+template <int EPI, int NMB>
+__global__ __launch_bounds__(256) void rowpair_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
+                                                           const bf16* __restrict__ W, int64_t ldw, int K,
+                                                           ppk::DecodeEpi ep) {
+    __shared__ f32x4 red[4][2][NMB][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lr = lane & 15, q4 = lane >> 4;
+    const int g = blockIdx.x;
+    int r0[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+        r0[nb] = EPI == ppk::kSwiGLU ? 32 * g + 16 * nb : (g >> 2) * 128 + 64 * nb + 16 * (g & 3);
+    const int kq = K / 4, k0 = w * kq, steps = kq / 32;
+    const bf16* wp[2];
+    const bf16* ap[NMB];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) wp[nb] = W + int64_t(r0[nb] + lr) * ldw + k0 + 8 * q4;
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) ap[mb] = A + int64_t(min(16 * mb + lr, k - 1)) * lda + k0 + 8 * q4;
+    bf16x8 rw[RP_RING][2], ra[RP_RING][NMB];
+    auto issue = [&](int u, int j) {
+        const int jj = 32 * min(j, steps - 1);
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) rw[u][nb] = *reinterpret_cast<const bf16x8*>(wp[nb] + jj);
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) ra[u][mb] = *reinterpret_cast<const bf16x8*>(ap[mb] + jj);
+    };
+#pragma unroll
+    for (int u = 0; u < RP_RING; ++u) issue(u, u);
+    f32x4 acc[2][NMB] = {};
+    for (int j0 = 0; j0 < steps; j0 += RP_RING) {
+#pragma unroll
+        for (int u = 0; u < RP_RING; ++u) {
+            if (j0 + u < steps) {
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+                    for (int mb = 0; mb < NMB; ++mb)
+                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rw[u][nb], ra[u][mb], acc[nb][mb], 0, 0, 0);
+            }
+            if (j0 + u + RP_RING < steps) issue(u, j0 + u + RP_RING);
+        }
+    }
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) red[w][nb][mb][lane] = acc[nb][mb];
+    __syncthreads();
+    for (int it = threadIdx.x; it < NMB * 64; it += 256) {
+        const int mb = it / 64, l = it % 64;
+        const int m = 16 * mb + (l & 15), c = 4 * (l >> 4);   // prompt, first of 4 rows of each block
+        if (m >= k) continue;
+        f32x4 a = red[0][0][mb][l], b = red[0][1][mb][l];
+#pragma unroll
+        for (int w2 = 1; w2 < 4; ++w2) {
+            a += red[w2][0][mb][l];
+            b += red[w2][1][mb][l];
+        }
+        if (EPI == ppk::kSwiGLU) {       // features 16 g + c .. + 3: gate a, up b
+            bf16x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(a[e]) * b[e]);
+            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + 16 * g + c) = o;
+        } else {                         // QKV: dims i .. i + 3 (a) and i + 64 .. (b) of head g / 4
+            const ppk::QkvOut& qo = ep.qkv;
+            const int head = g >> 2, i = 16 * (g & 3) + c;
+            const bool rotate = head < qo.H + qo.Hkv;
+            bf16x4 lo, hi;
+            if (rotate) {
+                const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float2 t = cs[e];
+                    lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
+                    hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    lo[e] = static_cast<bf16>(a[e]);
+                    hi[e] = static_cast<bf16>(b[e]);
+                }
+            }
+            bf16* dst;
+            if (head < qo.H)
+                dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
+            else
+                dst = static_cast<bf16*>(rotate ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
+                      (head - qo.H - (rotate ? 0 : qo.Hkv)) * 128;
+            *reinterpret_cast<bf16x4*>(dst + i) = lo;
+            *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+        }
+    }
+}
+
+template <int EPI>
+void launch_rowpair(int nmb, int N, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W, int64_t ldw,
+                    int K, const ppk::DecodeEpi& ep) {
+    const dim3 grid(N / 32);
+    switch (nmb) {
+        case 1: rowpair_gemm_kernel<EPI, 1><<<grid, 256, 0, s>>>(A, lda, k, W, ldw, K, ep); break;
+        case 2: rowpair_gemm_kernel<EPI, 2><<<grid, 256, 0, s>>>(A, lda, k, W, ldw, K, ep); break;
+        case 3: rowpair_gemm_kernel<EPI, 3><<<grid, 256, 0, s>>>(A, lda, k, W, ldw, K, ep); break;
+        default: rowpair_gemm_kernel<EPI, 4><<<grid, 256, 0, s>>>(A, lda, k, W, ldw, K, ep); break;
+    }
+}
+
 // Residual add of a split-K projection fused with the RMSNorm that follows it, one workgroup
 // of d / 4 threads per prompt row, 4 consecutive elements per thread: x[m] += sum over splits
 // of part[.][m] (split order; all S loads of a thread issued together), stored back; then
@@ -558,11 +676,13 @@ void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, 
 
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
                  const DecodeEpi& ep, hipStream_t s) {
-    const SkinnySplit sp = skinny_split(N, K);
-    const dim3 grid(N / SG_ROWS, sp.splits);
     const int nmb = (k + 15) / 16;
     const bf16* a = static_cast<const bf16*>(A);
     const bf16* w = static_cast<const bf16*>(W);
+    if (kRowPairs && epi == kSwiGLU) return launch_rowpair<kSwiGLU>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+    if (kRowPairs && epi == kQkvRope) return launch_rowpair<kQkvRope>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+    const SkinnySplit sp = skinny_split(N, K);
+    const dim3 grid(N / SG_ROWS, sp.splits);
     launch_skinny(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, part);
     if (epi == kResidual) return;   // the residual add happens in residual_rmsnorm
     const int64_t threads = int64_t(k) * (epi == kResidual ? N / 4 : N / 8);
