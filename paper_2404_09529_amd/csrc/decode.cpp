@@ -13,9 +13,9 @@
 //              the residual adds of O and down happen in the norm that follows each
 //   final rmsnorm (float32) -> LM head and greedy choice (the first-token kernels, one
 //   row per prompt).
-// The projections: for bf16 steps of up to 64 prompts, the skinny split-K GEMM with its
-// epilogue kernel (the weights are streamed from HBM by every CU); otherwise the prefill's
-// GEMM kernels with M = k rows.
+// The projections: for bf16 steps of up to 64 prompts, weight-streaming GEMMs for one row
+// per prompt (QKV and gate/up with their epilogues in the kernel; O and down as split-K
+// partial sums that the next norm adds); otherwise the prefill's GEMM kernels with M = k.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -87,7 +87,8 @@ Layout layout_of(const pp_config* c, const pp_gen_dlayout* g) {
     if (use_skinny(c, g->k)) {
         Proj p[4];
         projections(c, p);
-        for (const Proj& q : p) gpart = std::max(gpart, size_t(ppk::skinny_split(q.N, q.K).splits) * k * q.N * 4);
+        for (int i : {1, 3})   // O and down leave split-K partial sums
+            gpart = std::max(gpart, size_t(ppk::skinny_split(p[i].N, p[i].K).splits) * k * p[i].N * 4);
     }
     L.gpart = take(gpart);
     L.total = off;

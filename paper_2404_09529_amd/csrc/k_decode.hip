@@ -14,18 +14,20 @@
 //                        and all query heads of the group, so every key and value is read
 //                        from HBM once per step; it writes the chunk's (max, sum, output).
 // decode_combine_kernel  merges a prompt's chunk results in a fixed order.
-// skinny_gemm_kernel     the projections of a decode step, one row per prompt (k <= 64):
-//                        C[k, N] = A[k, K] W[N, K]^T is bound by streaming W from HBM, so
-//                        the work is cut into about 1024 pieces of 64 rows x a K split:
-//                        each workgroup stages its slice of A (k rows, LDS sized to k) once,
-//                        and each of its 4 wavefronts streams 16 rows of W straight from HBM
-//                        into registers, all its K steps requested up front, into the
-//                        16x16x32 bf16 MFMA (W rows x prompts); float32 partial sums per
-//                        split, added in split order by the kernel that consumes them.
-// decode_epilogue_kernel SwiGLU over the interleaved gate/up rows, or RoPE at the token's
-//                        position with the query store and the key/value append.
-// residual_rmsnorm_kernel  the residual add of the O and down projections fused with the
-//                        RMSNorm that follows each.
+// The projections of a decode step have one row per prompt (k <= 64): C[k, N] = A[k, K]
+// W[N, K]^T is bound by streaming W from HBM.
+// rowpair_gemm_kernel    QKV and gate/up: one workgroup per 32 weight rows whose epilogue
+//                        belongs together (rotate-half pairs; gate and up rows of the same
+//                        features), K split four ways across its wavefronts and added
+//                        through LDS; RoPE with the query store and the key/value append,
+//                        or SwiGLU, in the same kernel.
+// skinny_gemm_kernel     O and down (N = d, too few rows for one workgroup per 32): about
+//                        1024 pieces of 64 rows x a K split; each workgroup stages its slice
+//                        of A (k rows, LDS sized to k) once and each wavefront streams 16
+//                        weight rows into the 16x16x32 bf16 MFMA, all its K steps requested
+//                        up front; float32 partial sums per split.
+// residual_rmsnorm_kernel  adds those partial sums, in split order, to the residual stream
+//                        inside the RMSNorm that follows each projection.
 // (A single-kernel split-K with the sum done by the last workgroup of a row group was
 // measured slower: its cross-workgroup hand-off costs more than the launch it saves.)
 //
@@ -339,72 +341,6 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
     }
 }
 
-// Sum of the K splits of part at (m, n .. n + 3), in split order.
-__device__ __forceinline__ f32x4 split_sum(const float* part, int S, int k, int N, int m, int n) {
-    f32x4 v = *reinterpret_cast<const f32x4*>(part + int64_t(m) * N + n);
-    for (int s = 1; s < S; ++s) v += *reinterpret_cast<const f32x4*>(part + (int64_t(s) * k + m) * N + n);
-    return v;
-}
-
-// The split sums and the epilogue as a kernel of their own, one thread per 4 outputs.
-template <int EPI>
-__global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __restrict__ part, int S, int k, int N,
-                                                              ppk::DecodeEpi ep) {
-    const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
-    if (EPI == ppk::kResidual) {           // x[m][n] += sum
-        const int per = N / 4;
-        if (idx >= int64_t(k) * per) return;
-        const int m = static_cast<int>(idx / per), n = static_cast<int>(idx % per) * 4;
-        f32x4* x = reinterpret_cast<f32x4*>(static_cast<float*>(ep.out) + int64_t(m) * ep.ldo + n);
-        *x = *x + split_sum(part, S, k, N, m, n);
-    } else if (EPI == ppk::kSwiGLU) {      // out[m][f] = SiLU(gate) * up, gate/up rows interleaved by 16
-        const int F = N / 2, per = F / 4;
-        if (idx >= int64_t(k) * per) return;
-        const int m = static_cast<int>(idx / per), f = static_cast<int>(idx % per) * 4;
-        const int g = 32 * (f / 16) + f % 16;
-        const f32x4 gt = split_sum(part, S, k, N, m, g), up = split_sum(part, S, k, N, m, g + 16);
-        bf16x4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(gt[e]) * up[e]);
-        *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + f) = o;
-    } else {                               // QKV: RoPE on q and k (pairs i, i + 64), store / append
-        const ppk::QkvOut& qo = ep.qkv;
-        const int heads = qo.H + 2 * qo.Hkv, per = heads * 16;   // 16 pairs of quads per head of 128
-        if (idx >= int64_t(k) * per) return;
-        const int m = static_cast<int>(idx / per), r = static_cast<int>(idx % per);
-        const int head = r / 16, i = (r % 16) * 4;
-        const int n = head * 128 + i;
-        const f32x4 a = split_sum(part, S, k, N, m, n), b = split_sum(part, S, k, N, m, n + 64);
-        bf16x4 lo, hi;
-        const bool rotate = head < qo.H + qo.Hkv;
-        if (rotate) {
-            const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float2 t = cs[e];
-                lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
-                hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
-            }
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                lo[e] = static_cast<bf16>(a[e]);
-                hi[e] = static_cast<bf16>(b[e]);
-            }
-        }
-        bf16* dst;
-        if (head < qo.H) {
-            dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
-        } else {
-            dst = static_cast<bf16*>(rotate ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
-                  (head - qo.H - (rotate ? 0 : qo.Hkv)) * 128;
-        }
-        *reinterpret_cast<bf16x4*>(dst + i) = lo;
-        *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
-    }
-}
-
-
 // Decode projections whose epilogue needs two blocks of 16 weight rows together, SwiGLU (the
 // 16 gate rows and the 16 up rows of 16 features) and QKV (16 rotate-half pairs c, c + 64 of
 // a head): one workgroup per such 32 rows, its 4 wavefronts each taking a quarter of K, the
@@ -414,7 +350,6 @@ __global__ __launch_bounds__(256) void decode_epilogue_kernel(const float* __res
 // 8 (l / 16) of each 32-wide step; it ends with block nb's rows r_nb + 4 (l / 16) + 0..3 for
 // prompt 16 mb + l % 16.
 constexpr int RP_RING = 8;
-constexpr bool kRowPairs = true;   // SwiGLU and QKV projections: paired rows (true) or split-K + epilogue kernel
 
 template <int EPI, int NMB>
 __global__ __launch_bounds__(256) void rowpair_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
@@ -679,20 +614,11 @@ void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int6
     const int nmb = (k + 15) / 16;
     const bf16* a = static_cast<const bf16*>(A);
     const bf16* w = static_cast<const bf16*>(W);
-    if (kRowPairs && epi == kSwiGLU) return launch_rowpair<kSwiGLU>(nmb, N, s, a, lda, k, w, ldw, K, ep);
-    if (kRowPairs && epi == kQkvRope) return launch_rowpair<kQkvRope>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+    if (epi == kSwiGLU) return launch_rowpair<kSwiGLU>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+    if (epi == kQkvRope) return launch_rowpair<kQkvRope>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+    // kResidual: split-K partial sums, added to the residual stream by residual_rmsnorm
     const SkinnySplit sp = skinny_split(N, K);
-    const dim3 grid(N / SG_ROWS, sp.splits);
-    launch_skinny(sp.tiles_per_split, nmb, grid, s, a, lda, k, w, ldw, N, K, part);
-    if (epi == kResidual) return;   // the residual add happens in residual_rmsnorm
-    const int64_t threads = int64_t(k) * (epi == kResidual ? N / 4 : N / 8);
-    const int blocks = static_cast<int>((threads + 255) / 256);
-    if (epi == kResidual)
-        decode_epilogue_kernel<kResidual><<<blocks, 256, 0, s>>>(part, sp.splits, k, N, ep);
-    else if (epi == kSwiGLU)
-        decode_epilogue_kernel<kSwiGLU><<<blocks, 256, 0, s>>>(part, sp.splits, k, N, ep);
-    else
-        decode_epilogue_kernel<kQkvRope><<<blocks, 256, 0, s>>>(part, sp.splits, k, N, ep);
+    launch_skinny(sp.tiles_per_split, nmb, dim3(N / SG_ROWS, sp.splits), s, a, lda, k, w, ldw, N, K, part);
 }
 
 }  // namespace ppk

@@ -139,9 +139,9 @@ bool skinny_ok(int k, int N, int K);
 void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
                       float eps, hipStream_t s);
 
-// bf16 C = A W^T for k <= 64 rows (A [k, lda], W [N, ldw]) through float32 partial sums
-// (part: splits * k * N floats) and the epilogue `epi`: kSwiGLU or kQkvRope are applied by
-// a second kernel; kResidual leaves the partial sums for residual_rmsnorm to add.
+// bf16 C = A W^T for k <= 64 rows (A [k, lda], W [N, ldw]) with the epilogue `epi`:
+// kSwiGLU and kQkvRope in the GEMM kernel itself (N % 32 == 0); kResidual leaves float32
+// partial sums in part (splits * k * N floats) for residual_rmsnorm to add.
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
                  const DecodeEpi& ep, hipStream_t s);
 

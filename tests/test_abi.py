@@ -321,15 +321,15 @@ def test_decode_workspace_and_rejections(L):
     assert L.pp_decode_workspace_size(ctypes.byref(cfg), ctypes.byref(gl), ctypes.byref(n)) == pp.PP_OK
     k, d, H, D, F = 3, 4096, 32, 128, 14336
     chunks = 3 + 1                                          # ceil(300 / 128) context + 1 generated
-    # split-K partial sums of the one-row-per-prompt projections: about 1024 workgroups of 64
-    # rows x up to 4 tiles of 128 columns; the largest projection sets the size
+    # split-K partial sums of the O and down projections (one row per prompt): about 1024
+    # workgroups of 64 rows x up to 4 tiles of 128 columns; the larger one sets the size
     def splits(N, K):
         tiles, groups = K // 128, N // 64
         target = max(1, -(-1024 // groups))
         per = min(4, max(1, -(-tiles // target)))
         return -(-tiles // per)
     proj = [(48 * 128, d), (d, H * D), (2 * F, d), (d, F)]
-    gpart = max(splits(N, K) * k * N * 4 for N, K in proj)
+    gpart = max(splits(N, K) * k * N * 4 for N, K in (proj[1], proj[3]))   # O and down
     want = (k * d * 4 + k * d * 2 + k * H * D * 2 + k * H * D * 2 + k * F * 2 + k * d * 4
             + k * H * chunks * (D + 4) * 4 + k * 64 * 8 + (4 * k + 1) * 4 + 16 * d * 2 + 250 * k * 8
             + gpart)
