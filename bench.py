@@ -30,6 +30,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X published fp32 vector rate (packed FMA; with packed FP32 off,
+                            # as this library is built, one FMA per lane per clock caps it at 78.6)
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 METRIC = "effective prefill tokens/s + TFLOP/s (% bf16 MFMA peak) vs padded prefill"
 GEMM_SOURCE = os.path.join(ROOT, "paper_2404_09529_amd", "csrc", "k_gemm_bf16.hip")
@@ -575,21 +577,32 @@ def main():
     tflops = flops / (ms / 1e3) / 1e12
     log(f"packed: {ms:.3f} ms/step, {value:,.0f} tokens/s, {tflops:.1f} TFLOP/s effective")
 
-    # dominant kernel: the gate/up GEMM with the SwiGLU epilogue, same launch as inside pp_prefill
+    # dominant kernel: the gate/up GEMM (bf16: with the SwiGLU epilogue), same launch as inside
+    # pp_prefill; the float32 model's is the FMA (vector ALU) GEMM storing gate and up
     T, d, F = plan.n_slots, shape.d_model, shape.ffn_dim
+    bf = shape.dtype == "bf16"
+    peak = PEAK_BF16_TFLOPS if bf else PEAK_FP32_TFLOPS
     gen = torch.Generator(device="cuda").manual_seed(1)
-    A = torch.randn((T, d), generator=gen, device="cuda").to(torch.bfloat16)
-    Cb = torch.empty((T, F), dtype=torch.bfloat16, device="cuda")
-    Wgu = model.layers[0]["w_gateup"]
     kstream = torch.cuda.current_stream()
-    gemm = lambda: pp.pp_gemm(pp.PP_BF16, pp.PP_EPI_SWIGLU, A, d, Wgu, d, Cb, F, T, 2 * F, d, dplan, kstream)
+    Wgu = model.layers[0]["w_gateup"]
+    if bf:
+        A = torch.randn((T, d), generator=gen, device="cuda").to(torch.bfloat16)
+        Cb = torch.empty((T, F), dtype=torch.bfloat16, device="cuda")
+        gemm = lambda: pp.pp_gemm(pp.PP_BF16, pp.PP_EPI_SWIGLU, A, d, Wgu, d, Cb, F, T, 2 * F, d, dplan, kstream)
+        k_name, k_bytes = "gemm_bf16_kernel<kSwiGLU> (gate/up projection)", 2 * (case.total_len * d + 2 * F * d
+                                                                              + case.total_len * F)
+    else:
+        A = torch.randn((T, d), generator=gen, device="cuda")
+        Cb = torch.empty((T, 2 * F), dtype=torch.float32, device="cuda")
+        gemm = lambda: pp.pp_gemm(pp.PP_F32, pp.PP_EPI_STORE, A, d, Wgu, d, Cb, 2 * F, T, 2 * F, d, None, kstream)
+        k_name, k_bytes = "gemm_f32_kernel (gate/up projection)", 4 * (case.total_len * d + 2 * F * d
+                                                                        + case.total_len * 2 * F)
     kt = time_steps(gemm, args.kernel_launches, 3)
     k_flops = 2.0 * case.total_len * (2 * F) * d
     achieved = k_flops / (kt["ms_mean"] / 1e3) / 1e12
     del A, Cb
     log(f"gate/up GEMM: {kt['ms_mean']:.3f} ms/launch, {achieved:.1f} TFLOP/s algorithmic")
-    traffic = recorded_traffic()
-    k_bytes = 2 * (case.total_len * d + 2 * F * d + case.total_len * F)   # A, W once; C written once
+    traffic = recorded_traffic() if bf else None   # A, W once; C written once (k_bytes)
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -599,13 +612,14 @@ def main():
                    "k": int(len(lengths)), "capacity": int(case.capacity), "total_len": case.total_len,
                    "max_len": int(lengths.max()), "n_rows": plan.n_rows, "fill": round(case.total_len / plan.n_slots, 4)},
         "tflops_effective": round(tflops, 2), "frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "frac_peak": round(tflops / peak, 4), "peak_tflops": peak,
         "algorithmic_flop": flops,
         "ms_median": round(packed["ms_median"], 4), "ms_p10": round(packed["ms_p10"], 4),
         "ms_p90": round(packed["ms_p90"], 4),
         "pack_ms": round(pack_ms, 4), "plan_upload_ms": round(upload_ms, 3),
-        "roofline": {"kernel": "gemm_bf16_kernel<kSwiGLU> (gate/up projection)", "bound": "mfma",
-                     "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+        "roofline": {"kernel": k_name, "bound": "mfma" if bf else "alu",
+                     "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4),
                      "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
                      "ms_per_launch": round(kt["ms_mean"], 4),
                      "algorithmic_flop_per_launch": k_flops, "algorithmic_bytes_per_launch": k_bytes,

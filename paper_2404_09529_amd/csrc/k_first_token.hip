@@ -18,7 +18,7 @@
 
 namespace {
 
-constexpr int VB = 64;   // vocabulary rows per workgroup of the float32 kernel
+constexpr int VB = 1;    // vocabulary rows per workgroup of the float32 kernel
 
 struct ArgMax {
     float v;
@@ -186,30 +186,22 @@ __global__ __launch_bounds__(256) void lm_head_bf16_kernel(const bf16* __restric
     }
 }
 
-// float32 model: one thread per vocabulary row, prompts one after another.
-__global__ __launch_bounds__(VB) void lm_head_f32_kernel(const float* __restrict__ hl, int k, const float* __restrict__ W,
+// float32 model: one wavefront per vocabulary row (its lanes split d, the row read once,
+// coalesced), every prompt's logit reduced across the wavefront in a fixed order.
+__global__ __launch_bounds__(64) void lm_head_f32_kernel(const float* __restrict__ hl, int k, const float* __restrict__ W,
                                                          int V, int d, float* __restrict__ logits,
                                                          ArgMax* __restrict__ part) {
-    const int n = blockIdx.x * VB + threadIdx.x;
-    const float* w = W + int64_t(min(n, V - 1)) * d;
+    const int n = blockIdx.x, lane = threadIdx.x;
+    const float* w = W + int64_t(n) * d;
     for (int m = 0; m < k; ++m) {
         const float* h = hl + int64_t(m) * d;
         float s = 0.f;
-        for (int c = 0; c < d; ++c) s = fmaf(h[c], w[c], s);
-        float bv = -INFINITY;
-        int bi = INT32_MAX;
-        if (n < V) {
+        for (int c = lane; c < d; c += 64) s = fmaf(h[c], w[c], s);
+        s = wave_sum(s);
+        if (lane == 0) {
             if (logits) logits[int64_t(m) * V + n] = s;
-            bv = s;
-            bi = n;
+            part[int64_t(n) * k + m] = ArgMax{s, n};   // a NaN logit never wins the final reduction
         }
-#pragma unroll
-        for (int x = 1; x < 64; x <<= 1) {
-            const float ov = __shfl_xor(bv, x);
-            const int oi = __shfl_xor(bi, x);
-            if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-        }
-        if (threadIdx.x == 0) part[int64_t(blockIdx.x) * k + m] = ArgMax{bv, bi};
     }
 }
 
@@ -270,7 +262,7 @@ void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, i
     } else {
         float* hl = reinterpret_cast<float*>(ws);
         gather_last_kernel<float><<<k_pad, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);
-        lm_head_f32_kernel<<<n_blocks, VB, 0, s>>>(hl, k, static_cast<const float*>(lm_head), V, d, logits, part);
+        lm_head_f32_kernel<<<n_blocks, 64, 0, s>>>(hl, k, static_cast<const float*>(lm_head), V, d, logits, part);
     }
     argmax_finalize_kernel<<<k, 256, 0, s>>>(part, n_blocks, k, tokens);
 }
