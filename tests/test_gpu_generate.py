@@ -108,6 +108,9 @@ def _bf16_case(model_name, lengths, n_layers, seed=0):
     ("llama-1.3b", [37, 1, 300, 5, 129], 2, 4),
     ("mistral-7b", [64, 260, 3], 1, 3),
     ("llama-1.3b", [3] * 62 + [40, 9, 300, 1, 2, 7, 5, 3], 1, 2),   # over 64 prompts: the tiled GEMMs
+    ("llama-1.3b", [5, 17, 2] * 6 + [130, 1], 1, 2),                 # 20 prompts: two blocks of 16
+    ("mistral-7b", [4, 9, 1, 33] * 10, 1, 2),                        # 40 prompts: three blocks, GQA
+    ("llama-1.3b", [2, 11, 6, 1] * 16, 1, 2),                        # 64 prompts: four blocks
 ])
 def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     case = _bf16_case(model_name, lengths, n_layers)
