@@ -187,7 +187,7 @@ def _run_pack(lengths: Sequence[int], capacity: Optional[int], slot_cap=None, qt
     bs, bq = pp_plan_bounds(k, max(C, 0)) if C >= 0 else (0, 0)
     bs = bs if slot_cap is None else slot_cap
     bq = bq if qtile_cap is None else qtile_cap
-    arrs = {n: np.zeros(max(size, 1), dtype=np.int32) for n, size in
+    arrs = {n: np.empty(max(size, 1), dtype=np.int32) for n, size in
             [("row_seg_ptr", k + 1), ("seg_prompt", k), ("seg_start", k), ("seg_len", k),
              ("prompt_kv_off", k + 1), ("slot_seg", bs), ("slot_pos", bs), ("slot_kv", bs),
              ("qtile_seg", bq), ("qtile_q0", bq)]}
