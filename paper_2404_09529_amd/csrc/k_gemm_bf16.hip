@@ -304,7 +304,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
                                                           const bf16* __restrict__ B, int64_t ldb,
                                                           void* __restrict__ Cv, int64_t ldc, int M, int K,
                                                           const int32_t* __restrict__ slot_seg, int capacity,
-                                                          int tiles_m, int tiles_n, ppk::QkvOut qo) {
+                                                          int tiles_m, int tiles_n, int balanced, ppk::QkvOut qo) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
@@ -318,19 +318,37 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
     // each K slice of an activation or weight panel is fetched into the XCD's L2 once and
     // read there by every tile of the block.  Every XCD sweeps N at the same rate, so the
     // weight panels are also shared through the last-level cache.
+    //
+    // When tiles_m is not a multiple of 8 that split can leave one XCD a whole round of tiles
+    // more than the average; then (balanced != 0) the same group-ordered list is built over
+    // all M-tiles and cut into 8 contiguous ranges of equal length instead, one per XCD (a
+    // range may start inside a group, so two XCDs can share an activation panel).
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, n_slots = gridDim.x >> 3;
-    const int pm = (tiles_m + 7) / 8;
-    const int m_begin = xcd * pm, m_cnt = min(pm, tiles_m - m_begin);
-    if (m_cnt <= 0) return;
+    int m_begin, m_cnt, g_begin, n_local;
+    if (balanced) {
+        const int total = tiles_m * tiles_n, per = (total + 7) / 8;
+        m_begin = 0;
+        m_cnt = tiles_m;
+        g_begin = xcd * per;
+        n_local = min(per, total - g_begin);
+    } else {
+        const int pm = (tiles_m + 7) / 8;
+        m_begin = xcd * pm;
+        m_cnt = min(pm, tiles_m - m_begin);
+        g_begin = 0;
+        n_local = m_cnt * tiles_n;
+    }
+    if (m_cnt <= 0 || n_local <= 0) return;
     const int n_groups = (m_cnt + 7) / 8, gm = (m_cnt + n_groups - 1) / n_groups;
-    const int n_local = m_cnt * tiles_n;
     auto tile_m0 = [&](int local) {
-        const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
+        const int gi = g_begin + local;
+        const int group = gi / (gm * tiles_n), within = gi - group * gm * tiles_n;
         const int first = group * gm, gsz = min(m_cnt - first, gm);
         return (m_begin + first + within % gsz) * BM;
     };
     auto tile_n0 = [&](int local) {
-        const int group = local / (gm * tiles_n), within = local - group * gm * tiles_n;
+        const int gi = g_begin + local;
+        const int group = gi / (gm * tiles_n), within = gi - group * gm * tiles_n;
         const int first = group * gm, gsz = min(m_cnt - first, gm);
         return (within / gsz) * BN;
     };
@@ -530,10 +548,17 @@ void launch(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8) n = 8;
         return n / 8 * 8;
     }();
-    const int per_xcd = ((tiles_m + 7) / 8) * tiles_n;
-    const dim3 grid(8 * min(n_cu / 8, per_xcd));
+    // per-XCD tile count of the M-block split and of the balanced one; the balanced split is
+    // taken only when it saves a whole round of workgroups
+    const int wg_per_xcd = n_cu / 8;
+    const int blocked = ((tiles_m + 7) / 8) * tiles_n, even = (tiles_m * tiles_n + 7) / 8;
+    const auto rounds = [&](int t) { return (t + wg_per_xcd - 1) / wg_per_xcd; };
+    const int balanced = rounds(even) < rounds(blocked) ? 1 : 0;
+    const int per_xcd = balanced ? even : blocked;
+    const dim3 grid(8 * min(wg_per_xcd, per_xcd));
     gemm_bf16_kernel<EPI><<<grid, NT, kLds, s>>>(static_cast<const bf16*>(A), lda, static_cast<const bf16*>(B),
-                                                ldb, C, ldc, M, K, slot_seg, capacity, tiles_m, tiles_n, qo);
+                                                ldb, C, ldc, M, K, slot_seg, capacity, tiles_m, tiles_n, balanced,
+                                                qo);
 }
 
 }  // namespace
