@@ -187,9 +187,9 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
             const ppk::QkvOut qo{q, hd, gk, gv, kvw, table, slot_pos, slot_kv, H, Hkv};
             ppk::decode_gemm(ppk::kQkvRope, xn, d, k, w->wqkv[l], d, qkv_w, d, gpart,
                              ppk::DecodeEpi{nullptr, 0, qo}, s);
-            ppk::decode_attention(dt, q, hd, ck, cv, gk, gv, kvw, Ly, step, H, Hkv, D, part, attn, hd, s);
-            ppk::decode_gemm(ppk::kResidual, attn, hd, k, w->wo[l], hd, d, hd, gpart, ppk::DecodeEpi{x, d, qo},
-                             s);
+            ppk::decode_attention(dt, q, hd, ck, cv, gk, gv, kvw, Ly, step, H, Hkv, D, part, nullptr, hd, s);
+            const ppk::AttnChunks ac{part, g->ctx_span, step, Ly.n_ctx_chunks, Ly.n_ctx_chunks + Ly.n_gen_chunks, H};
+            ppk::decode_gemm_o(k, ac, w->wo[l], hd, d, hd, gpart, s);
             pending = ppk::skinny_split(d, hd).splits;
         } else if (bf) {
             const ppk::QkvOut qo{q, hd, gk, gv, kvw, table, slot_pos, slot_kv, H, Hkv};

@@ -13,7 +13,8 @@
 //                        A workgroup takes one (prompt, key/value head, chunk of 128 keys)
 //                        and all query heads of the group, so every key and value is read
 //                        from HBM once per step; it writes the chunk's (max, sum, output).
-// decode_combine_kernel  merges a prompt's chunk results in a fixed order.
+// decode_combine_kernel  merges a prompt's chunk results in a fixed order (on the paths that
+//                        do not merge them in the O projection's staging, below).
 // The projections of a decode step have one row per prompt (k <= 64): C[k, N] = A[k, K]
 // W[N, K]^T is bound by streaming W from HBM.
 // rowpair_gemm_kernel    QKV and gate/up: one workgroup per 32 weight rows whose epilogue
@@ -25,7 +26,8 @@
 //                        1024 pieces of 64 rows x a K split; each workgroup stages its slice
 //                        of A (k rows, LDS sized to k) once and each wavefront streams 16
 //                        weight rows into the 16x16x32 bf16 MFMA, all its K steps requested
-//                        up front; float32 partial sums per split.
+//                        up front; float32 partial sums per split.  For O the staged slice
+//                        is the attention output, merged there from the chunk results.
 // residual_rmsnorm_kernel  adds those partial sums, in split order, to the residual stream
 //                        inside the RMSNorm that follows each projection.
 // (A single-kernel split-K with the sum done by the last workgroup of a row group was
@@ -292,10 +294,10 @@ constexpr int SG_MAX_TILES = 4; // A tiles per K split
 // 8 (l / 16) of each 32-wide step, every step of its split requested before the first MFMA,
 // and holds, per prompt block mb, the sums of prompt 16 mb + l % 16 for rows
 // n_w + 4 (l / 16) + 0..3.  The slice of A (k_pad rows x NT tiles) is staged once in LDS.
-template <int NT, int NMB>
+template <int NT, int NMB, bool COMB>
 __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
                                                           const bf16* __restrict__ W, int64_t ldw, int N, int K,
-                                                          float* __restrict__ part) {
+                                                          float* __restrict__ part, ppk::AttnChunks ac) {
     extern __shared__ __attribute__((aligned(16))) char lds[];   // NT tiles of 16 NMB rows x 256 bytes
     constexpr int KP = 16 * NMB, TILE_B = KP * 256;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -309,11 +311,33 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
 #pragma unroll
     for (int j = 0; j < 4 * NT; ++j)
         if (j < 4 * nt) ring[j] = *reinterpret_cast<const bf16x8*>(wrow + 32 * j);
-    // stage A[0 .. KP) x tiles t0 .. t0 + nt (rows past k read as row k - 1, never stored)
+    // stage A[0 .. KP) x tiles t0 .. t0 + nt (rows past k read as row k - 1, never stored).
+    // COMB: A is the attention output, formed here from the decode attention's chunk results
+    // (128 columns = one head per tile): the chunks of prompt r and head t0 + t merged in
+    // the fixed order of decode_combine_kernel, divided by the sum, rounded to bf16.
     for (int idx = threadIdx.x; idx < KP * nt * 16; idx += 256) {
         const int r = idx / (nt * 16), q = idx % (nt * 16), t = q / 16, ch = q % 16;
-        const bf16x8 v = *reinterpret_cast<const bf16x8*>(A + int64_t(min(r, k - 1)) * lda +
-                                                          int64_t(t0 + t) * SG_TILE + ch * 8);
+        const int m = min(r, k - 1);
+        bf16x8 v;
+        if constexpr (COMB) {
+            constexpr int PS = 128 + 4;
+            const float* base = ac.part + (int64_t(m) * ac.H + t0 + t) * ac.n_chunks * PS;
+            const int nc = (ac.ctx_span[m] + CH - 1) / CH, ng = (ac.step + 1 + CH - 1) / CH;
+            float mm = -INFINITY, ll = 0.f, o[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = 0.f;
+            for (int c = 0; c < nc + ng; ++c) {
+                const float* pp = base + int64_t(c < nc ? c : ac.n_ctx_chunks + c - nc) * PS;
+                float o2[8];
+                load8(pp + ch * 8, o2);
+                merge<8>(mm, ll, o, pp[128], pp[129], o2);
+            }
+            const float inv = ll > 0.f ? 1.f / ll : 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = static_cast<bf16>(o[e] * inv);
+        } else {
+            v = *reinterpret_cast<const bf16x8*>(A + int64_t(m) * lda + int64_t(t0 + t) * SG_TILE + ch * 8);
+        }
         *reinterpret_cast<bf16x8*>(lds + t * TILE_B + r * 256 + 16 * (ch ^ gsw(r & 7))) = v;
     }
     // keep every W fragment in flight from the top: the compiler would otherwise sink each
@@ -508,25 +532,26 @@ __global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restric
     }
 }
 
-template <int NT>
+template <int NT, bool COMB>
 void launch_skinny_nt(int nmb, dim3 grid, size_t lds, hipStream_t s, const bf16* A, int64_t lda, int k,
-                      const bf16* W, int64_t ldw, int N, int K, float* part) {
+                      const bf16* W, int64_t ldw, int N, int K, float* part, const ppk::AttnChunks& ac) {
     switch (nmb) {
-        case 1: skinny_gemm_kernel<NT, 1><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
-        case 2: skinny_gemm_kernel<NT, 2><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
-        case 3: skinny_gemm_kernel<NT, 3><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
-        default: skinny_gemm_kernel<NT, 4><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part); break;
+        case 1: skinny_gemm_kernel<NT, 1, COMB><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part, ac); break;
+        case 2: skinny_gemm_kernel<NT, 2, COMB><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part, ac); break;
+        case 3: skinny_gemm_kernel<NT, 3, COMB><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part, ac); break;
+        default: skinny_gemm_kernel<NT, 4, COMB><<<grid, 256, lds, s>>>(A, lda, k, W, ldw, N, K, part, ac); break;
     }
 }
 
+template <bool COMB>
 void launch_skinny(int nt, int nmb, dim3 grid, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W,
-                   int64_t ldw, int N, int K, float* part) {
+                   int64_t ldw, int N, int K, float* part, const ppk::AttnChunks& ac) {
     const size_t lds = size_t(nt) * 16 * nmb * 256;
     switch (nt) {
-        case 1: launch_skinny_nt<1>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
-        case 2: launch_skinny_nt<2>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
-        case 3: launch_skinny_nt<3>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
-        default: launch_skinny_nt<4>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part); break;
+        case 1: launch_skinny_nt<1, COMB>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part, ac); break;
+        case 2: launch_skinny_nt<2, COMB>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part, ac); break;
+        case 3: launch_skinny_nt<3, COMB>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part, ac); break;
+        default: launch_skinny_nt<4, COMB>(nmb, grid, lds, s, A, lda, k, W, ldw, N, K, part, ac); break;
     }
 }
 
@@ -562,6 +587,7 @@ void attn_dispatch(int D, int R, const void* q, int64_t ldq, const void* ctx_k, 
     const int nch = Ly.n_ctx_chunks + Ly.n_gen_chunks;
     if (D == 128) {
         attn_by_group<T, 128>(R, q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, Ly, step, Hkv, part, s);
+        if (!out) return;   // the consumer merges the chunks itself
         decode_combine_kernel<T, 128><<<blocks, 256, 0, s>>>(part, Ly.k, H, Ly.ctx_span, step, Ly.n_ctx_chunks, nch,
                                                              static_cast<T*>(out), ldo);
     } else {
@@ -618,7 +644,16 @@ void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int6
     if (epi == kQkvRope) return launch_rowpair<kQkvRope>(nmb, N, s, a, lda, k, w, ldw, K, ep);
     // kResidual: split-K partial sums, added to the residual stream by residual_rmsnorm
     const SkinnySplit sp = skinny_split(N, K);
-    launch_skinny(sp.tiles_per_split, nmb, dim3(N / SG_ROWS, sp.splits), s, a, lda, k, w, ldw, N, K, part);
+    const AttnChunks none{};
+    launch_skinny<false>(sp.tiles_per_split, nmb, dim3(N / SG_ROWS, sp.splits), s, a, lda, k, w, ldw, N, K, part,
+                         none);
+}
+
+void decode_gemm_o(int k, const AttnChunks& ac, const void* W, int64_t ldw, int N, int K, float* part,
+                   hipStream_t s) {
+    const SkinnySplit sp = skinny_split(N, K);
+    launch_skinny<true>(sp.tiles_per_split, (k + 15) / 16, dim3(N / SG_ROWS, sp.splits), s, nullptr, 0, k,
+                        static_cast<const bf16*>(W), ldw, N, K, part, ac);
 }
 
 }  // namespace ppk

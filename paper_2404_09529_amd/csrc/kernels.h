@@ -108,11 +108,20 @@ struct DecodeLayout {
 void decode_prep(const DecodeLayout& Ly, int step, int D, float theta, float2* table, int32_t* slot_pos,
                  int32_t* slot_kv, int32_t* slot_seg, int32_t* ident, hipStream_t s);
 
+// The decode attention's per-chunk results (k x H x n_chunks x (D + 4) float32: o[D], max,
+// sum) and what is needed to merge a prompt's chunks.
+struct AttnChunks {
+    const float* part;
+    const int32_t* ctx_span;
+    int step, n_ctx_chunks, n_chunks, H;
+};
+
 // One query row per prompt (q [k, ldq], H heads of D) against the prompt's context rows
 // ctx_off[i] .. + ctx_span[i] of ctx_k / ctx_v (rows past ctx_valid[i] masked) and its
 // generated rows gen_off[i] .. + step of gen_k / gen_v; row stride ldkv; GQA head h reads
 // key/value head h / (H / Hkv).  out [k, ldo] = softmax(q k^T / sqrt(D)) v, dtype.
-// part: float32 scratch of k * H * (n_ctx_chunks + n_gen_chunks) * (D + 4).
+// part: float32 scratch of k * H * (n_ctx_chunks + n_gen_chunks) * (D + 4).  out == NULL:
+// the chunk results are left in part for decode_gemm_o to merge.
 // D in {64, 128}; H / Hkv in {1, 2, 4, 8}.
 void decode_attention(int dtype, const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v,
                       const void* gen_k, const void* gen_v, int64_t ldkv, const DecodeLayout& Ly, int step, int H,
@@ -133,6 +142,12 @@ struct SkinnySplit {
 SkinnySplit skinny_split(int N, int K);
 // Shapes the skinny GEMM takes: 1 <= k <= 64 rows, N % 64 == 0, K % 128 == 0.
 bool skinny_ok(int k, int N, int K);
+
+// The O projection of a decode step (bf16, head dim 128, k <= 64): its activations are the
+// attention output, merged from the attention's chunk results while they are staged; float32
+// split-K partial sums in part for residual_rmsnorm, as decode_gemm's kResidual.
+void decode_gemm_o(int k, const AttnChunks& ac, const void* W, int64_t ldw, int N, int K, float* part,
+                   hipStream_t s);
 
 // x[m] += sum of the S splits of part (split order; S = 0: nothing), stored back, then
 // out[m] = RMSNorm(x[m]) * g in dtype_out (PP_BF16 or PP_F32); k rows of d <= 4096.
