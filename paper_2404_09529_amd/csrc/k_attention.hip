@@ -20,6 +20,11 @@
 //     so the running max / sum of the online softmax (Milakov and Gimelshein 2018; the
 //     tiling of FlashAttention, Dao et al. 2022) are lane-local plus one exchange with the
 //     lane 32 away;
+//   * software pipeline with K one tile ahead of V: while the matrix cores compute the
+//     scores of key tile t + 1, the vector units turn the scores of tile t into bf16
+//     probabilities (exp2, row sums with dot2 on the rounded values), then P V of tile t
+//     follows; the exchange of row maxima and sums with the lane 32 away is a permlane32
+//     swap, so the softmax never waits on LDS;
 //   * the V operand of O^T += V^T P^T is read with the transposing LDS read
 //     (ds_read_b64_tr_b16), with key rows chosen so that its key order matches the order in
 //     which the S^T accumulators hold the probabilities: P feeds the MFMA from registers
@@ -112,21 +117,25 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
         koff[t] = pr * row_b + (col + 8 * (pc ^ kswz(pr))) * 2;
         voff[t] = pr * row_b + (col + 8 * (pc ^ vswz(pr))) * 2;
     }
-    auto issue = [&](int kt) {
-        char* stage = smem + (kt & 1) * STAGE_B;
+    // K tile kt goes to the first half of stage kt & 1, V tile kt to its second half.
+    auto tile_rsrc = [&](const bf16* base, int kt) {
         const int64_t first = int64_t(kv0) + kt * BKV;
         const int records = max(kv_rows - kt * BKV, 0) * row_b;
-        const __amdgpu_buffer_rsrc_t krsrc =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(kc + first * ldkv), 0, records, kRsrcWord3);
-        const __amdgpu_buffer_rsrc_t vrsrc =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(vc + first * ldkv), 0, records, kRsrcWord3);
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(base + first * ldkv), 0, records, kRsrcWord3);
+    };
+    auto issue_k = [&](int kt) {
+        char* dst = smem + (kt & 1) * STAGE_B;
+        const __amdgpu_buffer_rsrc_t r = tile_rsrc(kc, kt);
 #pragma unroll
-        for (int t = 0; t < LOADS; ++t) {
-            const int j = wave * LOADS + t;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, (lds_void*)(stage + j * 1024), 16, koff[t], 0, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(vrsrc, (lds_void*)(stage + TILE_B + j * 1024), 16, voff[t], 0,
-                                                     0, 0);
-        }
+        for (int t = 0; t < LOADS; ++t)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + (wave * LOADS + t) * 1024), 16, koff[t], 0, 0, 0);
+    };
+    auto issue_v = [&](int kt) {
+        char* dst = smem + (kt & 1) * STAGE_B + TILE_B;
+        const __amdgpu_buffer_rsrc_t r = tile_rsrc(vc, kt);
+#pragma unroll
+        for (int t = 0; t < LOADS; ++t)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + (wave * LOADS + t) * 1024), 16, voff[t], 0, 0, 0);
     };
 
     // ---- fragment addresses.  K: row b*32 + fr, chunk (2 ks + fh) ^ (fr & 15).  V (transposing
@@ -146,36 +155,83 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
     float m_i = -1e30f, l_i = 0.f;
     const float lazy = 8.0f / scale_log2;             // 8 in log2 units, as a raw-score margin
 
-    issue(0);
-    for (int kt = 0; kt < nkt; ++kt) {
-        __builtin_amdgcn_s_waitcnt(0x0f70);            // vmcnt(0): this wavefront's loads of tile kt
-        __builtin_amdgcn_s_barrier();                  // everyone's loads landed; stage of kt-1 free
-        __builtin_amdgcn_sched_barrier(0);
-        if (kt + 1 < nkt) issue(kt + 1);
-        const char* stage = smem + (kt & 1) * STAGE_B;
-        const int kb = kt * BKV;                       // first key of the tile
-        // every wavefront takes part in every key tile: one whose queries all precede the tile
-        // sees only masked scores (p = 0, corr = 1) and leaves o and l unchanged
-        // all K fragments of the tile first, then the 16 score MFMAs
-        bf16x8 kf[HD / 16][2];
+    // S^T of key tile kt: s[b][r] is the raw score of key 64 kt + 32 b + 8 (r / 4) + 4 fh + r % 4
+    // for this lane's query.  Every wavefront takes part in every key tile: one whose queries
+    // all precede the tile sees only masked scores (p = 0, corr = 1) and leaves o and l as
+    // they were.
+    auto scores = [&](int kt, f32x16 (&s)[2]) {
+        const char* kst = smem + (kt & 1) * STAGE_B;
 #pragma unroll
         for (int ks = 0; ks < HD / 16; ++ks)
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-                kf[ks][b] = *reinterpret_cast<const bf16x8*>(stage + k_lds + b * 32 * ROW + 16 * ((2 * ks) ^ kx));
-        __builtin_amdgcn_sched_barrier(0);
-        f32x16 s[2];
+            for (int b = 0; b < 2; ++b) {
+                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kst + k_lds + b * 32 * ROW + 16 * ((2 * ks) ^ kx));
+                s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], ks == 0 ? f32x16{} : s[b], 0, 0, 0);
+            }
+    };
+    // The mask (only the diagonal tile and the span's tail need it) and the online-softmax
+    // reference.  m_i is a per-lane reference maximum, kept unscaled; the scale 1/sqrt(D) (in
+    // log2 units) is folded into one FMA per score before the hardware exp2, and masked
+    // scores (-inf) give exactly 0.  The reference moves only when a score exceeds it by more
+    // than 8 in log2 units, so probabilities stay <= 2^8 and the output accumulators are
+    // rescaled only on those rare steps.  The exchange with the lane 32 away (the other half
+    // of the same query's keys) is a permlane32 swap: no LDS round trip.
+    auto reference = [&](int kt, f32x16 (&s)[2]) {
+        const int kb = kt * BKV;
+        if (kb + BKV - 1 > wq_lo || kb + BKV > n_kv) {
+            // key kb + 4 fh + off is allowed iff off <= lim (key <= qi and key < n_kv)
+            const int lim = min(qi, n_kv - 1) - (kb + 4 * fh);
 #pragma unroll
-        for (int ks = 0; ks < HD / 16; ++ks)
-#pragma unroll
             for (int b = 0; b < 2; ++b)
-                s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][b], qf[ks], ks == 0 ? f32x16{} : s[b], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        // the V operands of the whole tile are requested now, so their LDS latency hides behind
-        // the softmax.  Transposing read r of sub-step sub, d block db: this lane supplies the
-        // address of key row sub*16 + 8 r + vrow and d columns db*32 + vd .. +3 and receives
-        // 4 consecutive keys of one d.
-        bf16x8 vf[BKV / 16][HD / 32];
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (32 * b + 8 * (r >> 2) + (r & 3) > lim) s[b][r] = -INFINITY;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[b][r]);
+        const auto mw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(mw[0]), __uint_as_float(mw[1]));
+        if (__any(mx > m_i + lazy)) {
+            const float m_new = fmaxf(m_i, mx);
+            const float corr = __builtin_amdgcn_exp2f((m_i - m_new) * scale_log2);
+            l_i *= corr;
+#pragma unroll
+            for (int db = 0; db < HD / 32; ++db) o[db] *= corr;
+            m_i = m_new;
+        }
+    };
+    // P = exp2(scale s - scale m) rounded to bf16, in the order the PV MFMA takes it from
+    // registers (sub-step sub = keys 16 sub .. 16 sub + 15); l gains the sum of the rounded
+    // probabilities (two per dot2), so the normaliser matches the weights actually applied.
+    auto probs = [&](f32x16 (&s)[2], bf16x8 (&pf)[BKV / 16]) {
+        const float nm = -m_i * scale_log2;
+#pragma unroll
+        for (int sub = 0; sub < BKV / 16; ++sub)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                pf[sub][e] = static_cast<bf16>(__builtin_amdgcn_exp2f(fmaf(s[sub >> 1][(sub & 1) * 8 + e], scale_log2, nm)));
+        typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+        const bf16x2_t one2 = {static_cast<bf16>(1.0f), static_cast<bf16>(1.0f)};
+        float rs0 = 0.f, rs1 = 0.f;
+#pragma unroll
+        for (int sub = 0; sub < BKV / 16; ++sub)
+#pragma unroll
+            for (int e = 0; e < 8; e += 4) {
+                rs0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{pf[sub][e], pf[sub][e + 1]}, one2, rs0, false);
+                rs1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{pf[sub][e + 2], pf[sub][e + 3]}, one2, rs1, false);
+            }
+        float rs = rs0 + rs1;
+        const auto rw = __builtin_amdgcn_permlane32_swap(__float_as_uint(rs), __float_as_uint(rs), false, false);
+        l_i += __uint_as_float(rw[0]) + __uint_as_float(rw[1]);
+    };
+    // O^T += V^T P^T for key tile kt.  Transposing read r of sub-step sub, d block db: this lane
+    // supplies the address of key row sub*16 + 8 r + vrow and d columns db*32 + vd .. +3 and
+    // receives 4 consecutive keys of one d, in the order the S^T accumulators hold P.
+    auto pv = [&](int kt, const bf16x8 (&pf)[BKV / 16]) {
+        const char* vst = smem + (kt & 1) * STAGE_B + TILE_B;
 #pragma unroll
         for (int sub = 0; sub < BKV / 16; ++sub)
 #pragma unroll
@@ -185,65 +241,62 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
                 for (int r = 0; r < 2; ++r) {
                     const int row = sub * 16 + 8 * r + vrow;
                     const int d = db * 32 + vd;
-                    const char* p = stage + TILE_B + row * ROW + 16 * ((d >> 3) ^ vs) + (d & 7) * 2;
+                    const char* p = vst + row * ROW + 16 * ((d >> 3) ^ vs) + (d & 7) * 2;
                     v2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));   // generic -> LDS
                 }
-                vf[sub][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[sub], o[db], 0, 0, 0);
             }
+    };
+
+    // Software pipeline, K one tile ahead of V: step kt computes the scores of tile kt + 1 on
+    // the matrix cores while the vector units turn the scores of tile kt into probabilities,
+    // then accumulates P V of tile kt.  At the top of step kt this wavefront waits for its own
+    // loads of K(kt+1) and V(kt), and the barrier makes everyone's visible and frees the two
+    // halves read in step kt - 1 (K(kt) and V(kt-1)); those are refilled with K(kt+2) and
+    // V(kt+1).
+    auto step = [&](int kt, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
+        __builtin_amdgcn_s_waitcnt(0x0f70);            // vmcnt(0)
+        __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
-        // s[b][r] is the raw score of key kb + 32 b + 8 (r / 4) + 4 fh + r % 4 for this lane's
-        // query.  Only the diagonal tile and the span's tail need the predicate; it is
-        // applied in one branch per tile.
-        if (kb + BKV - 1 > wq_lo || kb + BKV > n_kv) {
-            // key kq + off is allowed iff off <= lim (key <= qi and key < n_kv)
-            const int lim = min(qi, n_kv - 1) - (kb + 4 * fh);
+        if (kt + 2 < nkt) issue_k(kt + 2);
+        if (kt + 1 < nkt) issue_v(kt + 1);
+        reference(kt, sc);
+        bf16x8 pf[BKV / 16];
+        if (kt + 1 < nkt) {
+            scores(kt + 1, sn);
+            probs(sc, pf);
+            // issue order: K fragments two steps ahead of their MFMAs, and ~6 vector
+            // instructions of the softmax after each score MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // DS reads
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (32 * b + 8 * (r >> 2) + (r & 3) > lim) s[b][r] = -INFINITY;
-        }
-        // online softmax on raw scores.  m_i is a per-lane reference maximum, kept unscaled;
-        // the scale 1/sqrt(D) (in log2 units) is folded into one FMA per score before the
-        // hardware exp2, and masked scores (-inf) give exactly 0.  The reference moves only
-        // when a score exceeds it by more than kLazy (2^8 in probability), so probabilities
-        // stay <= 2^8 and the output accumulators are rescaled only on those rare steps.
-        float mx = -INFINITY;
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[b][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-        if (__any(mx > m_i + lazy)) {
-            const float m_new = fmaxf(m_i, mx);
-            const float corr = __builtin_amdgcn_exp2f((m_i - m_new) * scale_log2);
-            l_i *= corr;
-#pragma unroll
-            for (int db = 0; db < HD / 32; ++db) o[db] *= corr;
-            m_i = m_new;
-        }
-        const float nm = -m_i * scale_log2;
-        float rs = 0.f;
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(s[b][r], scale_log2, nm));
-                s[b][r] = p;
-                rs += p;
+            for (int i = 0; i < HD / 16; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
             }
-        rs += __shfl_xor(rs, 32, kWave);
-        l_i += rs;
-#pragma unroll
-        for (int sub = 0; sub < BKV / 16; ++sub) {
-            bf16x8 pf;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(s[sub >> 1][(sub & 1) * 8 + e]);
-#pragma unroll
-            for (int db = 0; db < HD / 32; ++db)
-                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[sub][db], pf, o[db], 0, 0, 0);
+        } else {
+            probs(sc, pf);
         }
+        pv(kt, pf);
+    };
+
+    f32x16 sa[2], sb[2];
+    issue_k(0);
+    issue_v(0);
+    if (nkt > 1) issue_k(1);
+    __builtin_amdgcn_s_waitcnt(0x0f70);                // vmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    scores(0, sa);
+    int kt = 0;
+    for (; kt + 1 < nkt; kt += 2) {
+        step(kt, sa, sb);
+        step(kt + 1, sb, sa);
     }
+    if (kt < nkt) step(kt, sa, sb);
 
     if (!q_ok) return;
     const float inv_l = 1.0f / l_i;
