@@ -311,15 +311,20 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
 #pragma unroll
     for (int j = 0; j < 4 * NT; ++j)
         if (j < 4 * nt) ring[j] = *reinterpret_cast<const bf16x8*>(wrow + 32 * j);
-    // stage A[0 .. KP) x tiles t0 .. t0 + nt (rows past k read as row k - 1, never stored).
+    // stage A[0 .. KP) x tiles t0 .. t0 + nt (rows past k read as row k - 1, or zero when
+    // merged from chunks; their sums are never stored).
     // COMB: A is the attention output, formed here from the decode attention's chunk results
     // (128 columns = one head per tile): the chunks of prompt r and head t0 + t merged in
     // the fixed order of decode_combine_kernel, divided by the sum, rounded to bf16.
     for (int idx = threadIdx.x; idx < KP * nt * 16; idx += 256) {
         const int r = idx / (nt * 16), q = idx % (nt * 16), t = q / 16, ch = q % 16;
         const int m = min(r, k - 1);
-        bf16x8 v;
+        bf16x8 v{};
         if constexpr (COMB) {
+            if (r >= k) {   // padding rows of the tile: their sums are never stored
+                *reinterpret_cast<bf16x8*>(lds + t * TILE_B + r * 256 + 16 * (ch ^ gsw(r & 7))) = v;
+                continue;
+            }
             constexpr int PS = 128 + 4;
             const float* base = ac.part + (int64_t(m) * ac.H + t0 + t) * ac.n_chunks * PS;
             const int nc = (ac.ctx_span[m] + CH - 1) / CH, ng = (ac.step + 1 + CH - 1) / CH;
