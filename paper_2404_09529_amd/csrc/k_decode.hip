@@ -378,7 +378,7 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
 // from global memory into a ring of RP_RING steps.  Lane l: weight row r_nb + l % 16 and prompt 16 mb + l % 16, K offset
 // 8 (l / 16) of each 32-wide step; it ends with block nb's rows r_nb + 4 (l / 16) + 0..3 for
 // prompt 16 mb + l % 16.
-constexpr int RP_RING = 8;
+constexpr int RP_RING = 2;   // 2: 52 VGPRs; 4, 6 and 8 (132 VGPRs) measured 1-3% slower at the 7B shape
 
 template <int EPI, int NMB>
 __global__ __launch_bounds__(256) void rowpair_gemm_kernel(const bf16* __restrict__ A, int64_t lda, int k,
