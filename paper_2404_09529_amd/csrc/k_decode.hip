@@ -23,7 +23,7 @@
 //                        through LDS; RoPE with the query store and the key/value append,
 //                        or SwiGLU, in the same kernel.
 // skinny_gemm_kernel     O and down (N = d, too few rows for one workgroup per 32): about
-//                        1024 pieces of 64 rows x a K split; each workgroup stages its slice
+//                        512 pieces of 64 rows x a K split; each workgroup stages its slice
 //                        of A (k rows, LDS sized to k) once and each wavefront streams 16
 //                        weight rows into the 16x16x32 bf16 MFMA, all its K steps requested
 //                        up front; float32 partial sums per split.  For O the staged slice
@@ -624,7 +624,7 @@ void decode_attention(int dtype, const void* q, int64_t ldq, const void* ctx_k, 
 
 SkinnySplit skinny_split(int N, int K) {
     const int tiles = K / SG_TILE, groups = N / SG_ROWS;
-    const int target = std::max(1, (1024 + groups - 1) / groups);   // about 1024 workgroups
+    const int target = std::max(1, (512 + groups - 1) / groups);   // about 512 workgroups (1024, 2048: slower)
     const int per = std::min(SG_MAX_TILES, std::max(1, (tiles + target - 1) / target));
     return SkinnySplit{per, (tiles + per - 1) / per};
 }
