@@ -117,7 +117,9 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
     if constexpr (EPI == ppk::kResidual) {
         // C[m][nb0 ..] += this lane's accumulators, one 16-row block j at a time, staged
         // through LDS (16 rows x 128 floats, 512-byte rows) so that C is read and written as
-        // whole rows: instruction k covers rows 2 k and 2 k + 1, 16 bytes per lane.  The C
+        // whole rows: instruction k covers rows 2 k and 2 k + 1, 16 bytes per lane.  C moves
+        // with non-temporal loads and stores (it is touched once per tile; the O projection
+        // measured 3% faster, the down projection the same).  The C
         // rows of block j + 1 are requested before block j is stored: vmcnt counts stores and
         // completes in order, so a load issued after a store would wait for the store.
         // Staging row r's 16-byte chunk q sits at q ^ f(r), f = (r0 << 3) | (r1 << 2) | r2
@@ -132,7 +134,7 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
                 const int m = min(mb + 16 * j + 2 * k + half, M - 1);   // rows past M: read, not stored
-                buf[k] = *reinterpret_cast<const f32x4*>(C + int64_t(m) * ldc + col);
+                buf[k] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(C + int64_t(m) * ldc + col));
             }
         };
         load_block(0, cbuf[0]);
@@ -157,7 +159,8 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
                 const int m = mb + 16 * j + 2 * k + half;
-                if (m < M) *reinterpret_cast<f32x4*>(C + int64_t(m) * ldc + col) = v[k] + cbuf[j & 1][k];
+                if (m < M)
+                    __builtin_nontemporal_store(v[k] + cbuf[j & 1][k], reinterpret_cast<f32x4*>(C + int64_t(m) * ldc + col));
             }
         }
         // Wait for the stores too (and with them, vmcnt being in order, everything before
