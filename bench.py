@@ -10,6 +10,9 @@ Prints one JSON line:
   value            effective (non-pad) prefill tokens/s of the packed path
   tflops_effective algorithmic FLOP / time (pads and skipped work excluded)
   padded           the same kernels on the full-batching plan (the paper's baseline)
+  attention_pairs  causal (query, key) pairs per head and layer: algorithmic, and executed
+                   by the attention kernel (tile inflation); the padded plan's executed count
+                   sits under `padded`
   roofline         the dominant kernel (the gate/up projection GEMM with SwiGLU epilogue),
                    timed live with HIP events on its stream, against the bf16 MFMA peak;
                    `traffic` is its HBM bytes per launch from the committed counter summary,
@@ -52,6 +55,25 @@ def algorithmic_flops(shape, lengths):
                + 3 * s.d_model * s.ffn_dim)
     pairs = int(np.sum(np.asarray(lengths, dtype=np.int64) * (np.asarray(lengths, dtype=np.int64) + 1) // 2))
     return s.n_layers * (L * lin + 4 * s.n_heads * s.head_dim * pairs)
+
+
+def attention_pairs(plan, lengths, tiled=True, key_tile=64):
+    """Causal (query, key) pairs per head and layer: what the method needs, sum of l(l+1)/2,
+    and what the attention kernel computes.  The bf16 kernel (tiled) takes every query of a
+    work item's query tile against key tiles of 64 up to the tile's last query (section 3.2:
+    M' never leaves the prompt's diagonal block); the float32 kernel takes each real query's
+    own keys only."""
+    import numpy as np
+
+    from paper_2404_09529_amd import prepack as pp
+    L = np.asarray(lengths, dtype=np.int64)
+    alg = int((L * (L + 1) // 2).sum())
+    n = np.asarray(plan.seg_len, dtype=np.int64)[np.asarray(plan.qtile_seg, dtype=np.int64)]
+    q0 = np.asarray(plan.qtile_q0, dtype=np.int64)
+    qt = pp.PP_QTILE
+    n_kv = np.minimum(q0 + qt, n)
+    exe = int((qt * key_tile * ((n_kv + key_tile - 1) // key_tile)).sum()) if tiled else alg
+    return {"algorithmic": alg, "executed": exe, "inflation": round(exe / max(alg, 1), 3)}
 
 
 def time_steps(fn, steps, warmup):
@@ -617,6 +639,7 @@ def main():
         "ms_median": round(packed["ms_median"], 4), "ms_p10": round(packed["ms_p10"], 4),
         "ms_p90": round(packed["ms_p90"], 4),
         "pack_ms": round(pack_ms, 4), "plan_upload_ms": round(upload_ms, 3),
+        "attention_pairs": attention_pairs(plan, lengths, tiled=bf),
         "roofline": {"kernel": k_name, "bound": "mfma" if bf else "alu",
                      "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
@@ -655,7 +678,8 @@ def main():
         pms = padded["ms_mean"]
         out["padded"] = {"ms_per_step": round(pms, 4), "tokens_per_s": round(case.total_len / (pms / 1e3), 1),
                          "tflops_effective": round(flops / (pms / 1e3) / 1e12, 2), "n_rows": pplan.n_rows,
-                         "capacity": pplan.capacity}
+                         "capacity": pplan.capacity,
+                         "attention_pairs_executed": attention_pairs(pplan, lengths, tiled=bf)["executed"]}
         out["speedup_vs_padded"] = round(pms / ms, 3)
         log(f"padded: {pms:.3f} ms/step, speedup {pms / ms:.2f}x")
         del pstep
