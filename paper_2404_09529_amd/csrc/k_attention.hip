@@ -91,7 +91,6 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
     const int qi = q0 + wave * 32 + fr;               // this lane's query (offset in the segment)
     const bool q_ok = qi < n;
     const int wq_lo = q0 + wave * 32;
-    const int wq_hi = min(wq_lo + 31, n - 1);
 
     bf16x8 qf[HD / 16];
     {
