@@ -127,3 +127,23 @@ def test_linear_fit_of_a_constant_predictor_is_none():
     # batch size 1: every batch has r/k = 1
     assert bench.linear_fit([1.0, 1.0, 1.0], [0.99, 1.0, 1.01]) is None
     assert bench.linear_fit([0.5, 0.6, 0.7], [1.0, 1.0, 1.0]) is None
+
+
+def test_attention_pairs_brute_force():
+    # causal pairs per head and layer, counted one by one on a tiny plan: the method needs
+    # l(l+1)/2 per prompt; the tiled kernel computes each work item's whole query tile
+    # against key tiles of 64 up to the item's last key
+    lengths = [1, 130, 64, 300]
+    plan = pp.pp_pack(lengths, 512)
+    got = bench.attention_pairs(plan, lengths)
+    want_alg = sum(1 for n in lengths for q in range(n) for key in range(q + 1))
+    want_exe = 0
+    for s, q0 in zip(plan.qtile_seg.tolist(), plan.qtile_q0.tolist()):
+        n = int(plan.seg_len[s])
+        last_key = min(q0 + pp.PP_QTILE, n) - 1
+        want_exe += sum(1 for q in range(pp.PP_QTILE) for key in range(64 * (last_key // 64 + 1)))
+    assert got["algorithmic"] == want_alg
+    assert got["executed"] == want_exe
+    assert got["inflation"] >= 1.0
+    # the float32 kernel takes each real query's own keys only
+    assert bench.attention_pairs(plan, lengths, tiled=False)["executed"] == want_alg
