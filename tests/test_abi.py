@@ -322,11 +322,11 @@ def test_decode_workspace_and_rejections(L):
     k, d, H, D, F = 3, 4096, 32, 128, 14336
     chunks = 3 + 1                                          # ceil(300 / 128) context + 1 generated
     # split-K partial sums of the O and down projections (one row per prompt): about 512
-    # workgroups of 64 rows x up to 4 tiles of 128 columns; the larger one sets the size
+    # workgroups of 64 rows x up to 6 tiles of 128 columns; the larger one sets the size
     def splits(N, K):
         tiles, groups = K // 128, N // 64
         target = max(1, -(-512 // groups))
-        per = min(4, max(1, -(-tiles // target)))
+        per = min(6, max(1, -(-tiles // target)))
         return -(-tiles // per)
     proj = [(48 * 128, d), (d, H * D), (2 * F, d), (d, F)]
     gpart = max(splits(N, K) * k * N * 4 for N, K in (proj[1], proj[3]))   # O and down
