@@ -111,6 +111,7 @@ def _bf16_case(model_name, lengths, n_layers, seed=0):
     ("llama-1.3b", [5, 17, 2] * 6 + [130, 1], 1, 2),                 # 20 prompts: two blocks of 16
     ("mistral-7b", [4, 9, 1, 33] * 10, 1, 2),                        # 40 prompts: three blocks, GQA
     ("llama-1.3b", [2, 11, 6, 1] * 16, 1, 2),                        # 64 prompts: four blocks
+    ("mistral-7b", [3, 8, 1, 20] * 16, 1, 2),                        # 64 prompts, d 4096: 96 KB staged slice
 ])
 def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     case = _bf16_case(model_name, lengths, n_layers)
