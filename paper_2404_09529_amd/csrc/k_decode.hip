@@ -26,9 +26,9 @@
 //                        512 pieces of 64 rows x a K split of up to 6 tiles of 128; each
 //                        workgroup stages its slice of A (k rows, LDS sized to k) once and
 //                        each wavefront streams 16 weight rows into the 16x16x32 bf16 MFMA,
-//                        all its K steps requested
-//                        up front; float32 partial sums per split.  For O the staged slice
-//                        is the attention output, merged there from the chunk results.
+//                        all its K steps requested up front; float32 partial sums per
+//                        split.  For O the staged slice is the attention output, merged
+//                        there from the chunk results.
 // residual_rmsnorm_kernel  adds those partial sums, in split order, to the residual stream
 //                        inside the RMSNorm that follows each projection.
 // (A single-kernel split-K with the sum done by the last workgroup of a row group was
@@ -376,9 +376,9 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
 // a head): one workgroup per such 32 rows, its 4 wavefronts each taking a quarter of K, the
 // quarters added in wavefront order through LDS and the epilogue applied in the same kernel
 // (no partial sums leave the workgroup).  Weight and activation fragments are read straight
-// from global memory into a ring of RP_RING steps.  Lane l: weight row r_nb + l % 16 and prompt 16 mb + l % 16, K offset
-// 8 (l / 16) of each 32-wide step; it ends with block nb's rows r_nb + 4 (l / 16) + 0..3 for
-// prompt 16 mb + l % 16.
+// from global memory into a ring of RP_RING steps.  Lane l: weight row r_nb + l % 16 and
+// prompt 16 mb + l % 16, K offset 8 (l / 16) of each 32-wide step; it ends with block nb's
+// rows r_nb + 4 (l / 16) + 0..3 for prompt 16 mb + l % 16.
 constexpr int RP_RING = 2;   // 2: 52 VGPRs; 4, 6 and 8 (132 VGPRs) measured 1-3% slower at the 7B shape
 
 template <int EPI, int NMB>
