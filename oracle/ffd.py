@@ -39,10 +39,6 @@ from typing import List, Optional, Sequence
 
 import numpy as np
 
-# attention query-tile length used by the work list in the plan; a scheduling
-# unit of the GPU kernels, not part of the method.  Kept equal to the library's.
-QTILE = 128
-
 
 def ffd(lengths: Sequence[int], capacity: int) -> List[List[int]]:
     """First-fit decreasing.  Returns bins as lists of prompt indices in placement order."""
@@ -126,16 +122,10 @@ class Plan:
     slot_seg: np.ndarray       # [n_rows * capacity], -1 outside every span
     slot_pos: np.ndarray       # [n_rows * capacity], 0 outside every span
     slot_kv: np.ndarray        # [n_rows * capacity], -1 at pads
-    qtile_seg: np.ndarray      # [n_qtiles]
-    qtile_q0: np.ndarray       # [n_qtiles]
 
     @property
     def n_slots(self) -> int:
         return self.n_rows * self.capacity
-
-    @property
-    def n_qtiles(self) -> int:
-        return int(self.qtile_seg.size)
 
 
 def _prefix(lengths: np.ndarray) -> np.ndarray:
@@ -145,28 +135,12 @@ def _prefix(lengths: np.ndarray) -> np.ndarray:
     return off
 
 
-def _qtiles(seg_len: np.ndarray, qtile: int):
-    """Attention work list: every (span, query offset) tile, most key work first.
-
-    Key work of a tile = number of keys its last query sees; ties keep span
-    order then offset order.  Only the set of tiles is part of the contract;
-    the order is a load-balancing heuristic (longest processing time first).
-    """
-    tiles = []
-    for s, n in enumerate(seg_len):
-        for q0 in range(0, int(n), qtile):
-            tiles.append((min(q0 + qtile, int(n)), s, q0))
-    tiles.sort(key=lambda t: (-t[0], t[1], t[2]))
-    return (np.array([t[1] for t in tiles], dtype=np.int32),
-            np.array([t[2] for t in tiles], dtype=np.int32))
-
-
 def _check_lengths(lengths: np.ndarray) -> None:
     if np.any(lengths <= 0):
         raise ValueError("every prompt needs at least one token")
 
 
-def pack(lengths: Sequence[int], capacity: int = 0, qtile: int = QTILE) -> Plan:
+def pack(lengths: Sequence[int], capacity: int = 0) -> Plan:
     """Algorithm 1 up to the model call: BINPACK, TENSORIZE layout, RESTART-PE, UNPACK map."""
     lengths = np.asarray(lengths, dtype=np.int64)
     k = len(lengths)
@@ -199,15 +173,14 @@ def pack(lengths: Sequence[int], capacity: int = 0, qtile: int = QTILE) -> Plan:
             slot_seg[a + j] = s
             slot_pos[a + j] = j                 # restart positions
             slot_kv[a + j] = off[p] + j         # UNPACK target row
-    qs, q0 = _qtiles(np.array(seg_len, dtype=np.int64), qtile)
     return Plan(k=k, capacity=C, n_rows=r, max_len=m, total_len=int(off[-1]),
                 row_seg_ptr=row_seg_ptr, seg_prompt=np.array(seg_prompt, dtype=np.int32),
                 seg_start=np.array(seg_start, dtype=np.int32),
                 seg_len=np.array(seg_len, dtype=np.int32), prompt_kv_off=off.astype(np.int32),
-                slot_seg=slot_seg, slot_pos=slot_pos, slot_kv=slot_kv, qtile_seg=qs, qtile_q0=q0)
+                slot_seg=slot_seg, slot_pos=slot_pos, slot_kv=slot_kv)
 
 
-def pack_padded(lengths: Sequence[int], qtile: int = QTILE) -> Plan:
+def pack_padded(lengths: Sequence[int]) -> Plan:
     """Full batching (section 4.2): prompt i alone in row i, right-padded to m.
 
     Row i is one causal span of length m starting at slot i*m; positions run
@@ -230,13 +203,12 @@ def pack_padded(lengths: Sequence[int], qtile: int = QTILE) -> Plan:
             if j < lengths[i]:
                 slot_kv[i * m + j] = off[i] + j
     seg_len = np.full(k, m, dtype=np.int32)
-    qs, q0 = _qtiles(seg_len.astype(np.int64), qtile)
     return Plan(k=k, capacity=m, n_rows=k, max_len=m, total_len=int(off[-1]),
                 row_seg_ptr=np.arange(k + 1, dtype=np.int32),
                 seg_prompt=np.arange(k, dtype=np.int32),
                 seg_start=(np.arange(k, dtype=np.int64) * m).astype(np.int32),
                 seg_len=seg_len, prompt_kv_off=off.astype(np.int32),
-                slot_seg=slot_seg, slot_pos=slot_pos, slot_kv=slot_kv, qtile_seg=qs, qtile_q0=q0)
+                slot_seg=slot_seg, slot_pos=slot_pos, slot_kv=slot_kv)
 
 
 def independent_mask(plan: Plan, row: int) -> np.ndarray:

@@ -14,8 +14,11 @@ from oracle import ffd
 from paper_2404_09529_amd import prepack as pp
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+# the plan fields the paper defines (Algorithm 1; sections 3.1 and 3.2), compared bit for bit
+# with the oracle; the attention work list is a scheduling choice of the library, checked by
+# its own invariants (_check_work_list)
 FIELDS = ("row_seg_ptr", "seg_prompt", "seg_start", "seg_len", "prompt_kv_off", "slot_seg", "slot_pos",
-          "slot_kv", "qtile_seg", "qtile_q0")
+          "slot_kv")
 
 
 @pytest.fixture(scope="module")
@@ -49,11 +52,22 @@ def test_version(L):
     assert "gfx950" in pp.pp_version()
 
 
+def _check_work_list(plan):
+    """The attention work list as include/prepack.h states it: every (segment, multiple of
+    PP_QTILE below the segment's length) exactly once, tiles with more keys to visit first."""
+    got = sorted(zip(plan.qtile_seg.tolist(), plan.qtile_q0.tolist()))
+    want = sorted((s, q0) for s in range(plan.k) for q0 in range(0, int(plan.seg_len[s]), pp.PP_QTILE))
+    assert got == want
+    keys = [min(q0 + pp.PP_QTILE, int(plan.seg_len[s])) for s, q0 in zip(plan.qtile_seg, plan.qtile_q0)]
+    assert all(a >= b for a, b in zip(keys, keys[1:]))
+
+
 def _same(plan, ref):
     for s in ("k", "capacity", "n_rows", "max_len", "total_len"):
         assert getattr(plan, s) == getattr(ref, s), s
     for f in FIELDS:
         assert np.array_equal(getattr(plan, f), getattr(ref, f)), f
+    _check_work_list(plan)
 
 
 def test_golden_examples(L, golden_dir):

@@ -71,7 +71,7 @@ def test_special_cases():
     assert ffd.pack([5, 5, 5]).n_rows == 3
     # empty batch
     p = ffd.pack([], 16)
-    assert p.n_rows == 0 and p.total_len == 0 and p.n_qtiles == 0
+    assert p.n_rows == 0 and p.total_len == 0
     # invalid inputs
     with pytest.raises(ValueError):
         ffd.pack([3, 0, 2], 8)
@@ -105,12 +105,6 @@ def _check_plan_invariants(lengths, p):
         assert np.array_equal(p.slot_pos[a:a + n], np.arange(n))
         assert np.array_equal(p.slot_kv[a:a + n], p.prompt_kv_off[i] + np.arange(n))
         assert np.all(p.slot_seg[a:a + n] == s)
-    # work list covers every (span, q0) exactly once, heaviest first
-    tiles = sorted(zip(p.qtile_seg.tolist(), p.qtile_q0.tolist()))
-    want = sorted((s, q0) for s in range(k) for q0 in range(0, int(p.seg_len[s]), ffd.QTILE))
-    assert tiles == want
-    work = [min(q0 + ffd.QTILE, int(p.seg_len[s])) for s, q0 in zip(p.qtile_seg, p.qtile_q0)]
-    assert all(a >= b for a, b in zip(work, work[1:]))
 
 
 @settings(max_examples=200, deadline=None)
