@@ -118,7 +118,8 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, allowed: np.ndarray,
               rnd: Rounder = _ident, q_chunk: int = 2048) -> np.ndarray:
     """softmax(q k^T / sqrt(D) + mask) v per head.
 
-    q [n, H, D]; k, v [n, Hkv, D]; allowed [n, n] boolean (query, key).
+    q [nq, H, D]; k, v [n, Hkv, D]; allowed: [nq, n] boolean (query, key), or anything
+    sliced like it.
     Rows are processed in chunks of ``q_chunk`` queries to bound memory; every
     row's arithmetic is the same whatever the chunking.
     """
@@ -149,6 +150,19 @@ def causal(n: int) -> np.ndarray:
     return np.tril(np.ones((n, n), dtype=bool))
 
 
+class CausalRows:
+    """The causal mask of n tokens, produced a block of query rows at a time instead of as
+    one [n, n] array: ``CausalRows(n)[rows]`` equals ``causal(n)[rows]`` for a slice or an
+    index array.  Long prompts (tens of thousands of tokens) need it to stay in memory."""
+
+    def __init__(self, n: int):
+        self.n = n
+
+    def __getitem__(self, rows) -> np.ndarray:
+        q = np.arange(self.n)[rows]
+        return np.arange(self.n)[None, :] <= q[:, None]
+
+
 # ----------------------------------------------------------------------------- the stack
 @dataclass
 class Result:
@@ -158,8 +172,16 @@ class Result:
 
 
 def forward(x: np.ndarray, weights: Dict, shape: Shape, positions: np.ndarray,
-            allowed: np.ndarray, rnd: Rounder = _ident, dtype=np.float64) -> Result:
-    """The decoder over one sequence of embedded tokens x [n, d]."""
+            allowed, rnd: Rounder = _ident, dtype=np.float64,
+            last_rows: Optional[np.ndarray] = None) -> Result:
+    """The decoder over one sequence of embedded tokens x [n, d].
+
+    ``allowed`` is the [n, n] boolean mask (query, key), or anything indexed like it
+    (``CausalRows``).  ``last_rows`` (default: all) restricts what the LAST layer computes
+    after its keys and values to those query rows: their attention output, MLP and final
+    norm.  Every layer's keys and values, and every result at those rows, are the same as
+    without the restriction, since no other row reads them; ``hidden`` then holds only those
+    rows, in the order given."""
     s = shape
     H, Hkv, D = s.n_heads, s.n_kv_heads, s.head_dim
     n = x.shape[0]
@@ -168,15 +190,22 @@ def forward(x: np.ndarray, weights: Dict, shape: Shape, positions: np.ndarray,
     cos, sin = cos.astype(dtype), sin.astype(dtype)
     ks, vs = [], []
     eps = dtype(s.rms_eps)
-    for L in weights["layers"][: s.n_layers]:
+    layers = weights["layers"][: s.n_layers]
+    for li, L in enumerate(layers):
         W = {key: np.asarray(val, dtype=dtype) for key, val in L.items()}
         xn = rnd(rms_norm(x, W["attn_norm"], eps))
-        q = rnd(xn @ W["wq"].T).reshape(n, H, D)
         k = rnd(xn @ W["wk"].T).reshape(n, Hkv, D)
         v = rnd(xn @ W["wv"].T).reshape(n, Hkv, D)
-        q = rnd(rope(q, cos, sin))
         k = rnd(rope(k, cos, sin))
-        o = rnd(attention(q, k, v, allowed, rnd).reshape(n, H * D))
+        if last_rows is not None and li == len(layers) - 1:
+            sel = np.asarray(last_rows, dtype=np.int64)
+            xn, x, qcos, qsin, mask = xn[sel], x[sel], cos[sel], sin[sel], allowed[sel]
+        else:
+            qcos, qsin, mask = cos, sin, allowed
+        nq = x.shape[0]
+        q = rnd(xn @ W["wq"].T).reshape(nq, H, D)
+        q = rnd(rope(q, qcos, qsin))
+        o = rnd(attention(q, k, v, mask, rnd).reshape(nq, H * D))
         x = x + o @ W["wo"].T
         hn = rnd(rms_norm(x, W["mlp_norm"], eps))
         a = rnd(silu(hn @ W["wg"].T) * (hn @ W["wu"].T))
@@ -199,10 +228,11 @@ def _alloc(total: int, shape: Shape, dtype) -> Result:
 
 
 def prefill_prompt(tokens: np.ndarray, weights: Dict, shape: Shape, rnd: Rounder = _ident,
-                   dtype=np.float64) -> Result:
-    """One prompt alone: causal mask, positions 0..l-1."""
+                   dtype=np.float64, last_rows: Optional[np.ndarray] = None) -> Result:
+    """One prompt alone: causal mask, positions 0..l-1.  ``last_rows`` as in ``forward``."""
     n = len(tokens)
-    return forward(embed(weights, tokens, dtype), weights, shape, np.arange(n), causal(n), rnd, dtype)
+    return forward(embed(weights, tokens, dtype), weights, shape, np.arange(n), CausalRows(n), rnd, dtype,
+                   last_rows)
 
 
 def prefill_per_prompt(lengths: Sequence[int], tokens: np.ndarray, weights: Dict, shape: Shape,

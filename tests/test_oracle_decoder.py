@@ -213,3 +213,37 @@ def test_round_bf16():
     want = np.array([1.0, 1.0, 1.0 + 2.0 ** -6, -2.5, 1.0 + 2.0 ** -7, 226 / 128 * 2.0 ** 127])
     got = D.round_bf16(x)
     assert np.array_equal(got, want)
+
+
+# ----------------------------------------------------------------------------- long-prompt helpers
+def test_causal_rows_equal_the_dense_causal_mask():
+    n = 11
+    dense = D.causal(n)
+    lazy = D.CausalRows(n)
+    assert np.array_equal(lazy[0:n], dense)
+    assert np.array_equal(lazy[3:7], dense[3:7])
+    idx = np.array([10, 0, 4, 4])
+    assert np.array_equal(lazy[idx], dense[idx])
+
+
+@pytest.mark.parametrize("n_layers", [1, 2])
+@pytest.mark.parametrize("shape", [TINY, TINY_GQA], ids=["mha", "gqa"])
+def test_last_layer_rows_match_hugging_face_and_the_full_pass(n_layers, shape):
+    """Restricting the last layer to a few query rows (what the long-prompt GPU tests use)
+    gives Hugging Face's hidden states at those rows and leaves every cache row unchanged."""
+    c = _case([23], n_layers=n_layers, **shape)
+    sh = D.Shape.of(c.shape)
+    rows = np.array([22, 0, 7, 15, 16])
+    part = D.prefill_prompt(c.tokens, c.weights, sh, last_rows=rows)
+    full = D.prefill_prompt(c.tokens, c.weights, sh)
+    h, ks, vs = hf_llama.run(hf_llama.build(c.shape, c.weights), c.tokens[None, :])
+    assert part.hidden.shape == (len(rows), sh.d_model)
+    assert D.errors(part.hidden, h[0][rows])[0] < 1e-5
+    assert D.errors(part.hidden, full.hidden[rows])[0] < 1e-12
+    for l in range(n_layers):
+        assert D.errors(part.k[l], ks[l][0])[0] < 1e-5 and D.errors(part.v[l], vs[l][0])[0] < 1e-5
+        assert np.array_equal(part.k[l], full.k[l]) and np.array_equal(part.v[l], full.v[l])
+    # the bf16 rounding hook sees the same values at those rows
+    part_r = D.prefill_prompt(c.tokens, c.weights, sh, rnd=D.round_bf16, last_rows=rows)
+    full_r = D.prefill_prompt(c.tokens, c.weights, sh, rnd=D.round_bf16)
+    assert D.errors(part_r.hidden, full_r.hidden[rows])[0] < 1e-12
