@@ -8,8 +8,8 @@ against the generation oracle (full recomputation per token, section 2.2).
   one row per prompt, beyond that the prefill's tiled GEMMs): every pp_decode_step is fed
   the oracle's token, and the rows
   it appends to the cache and its logits are gated against the error of an ideal bf16
-  pipeline (the oracle with every stored value rounded to bf16), as the prefill's parity
-  is; its token must be the oracle's where the oracle's lead exceeds twice the logit error,
+  pipeline (the oracle with every stored value rounded to bf16): max and mean error each
+  <= 1.25x the floor's, as in the prefill's parity; its token must be the oracle's where the oracle's lead exceeds twice the logit error,
   else a valid argmax.
 * the packed and the full-batching layouts give bit-identical tokens and generated rows,
   and pp_generate is bit-identical to the same steps taken one by one.
@@ -23,7 +23,7 @@ from oracle import generate as G
 from paper_2404_09529_amd import prepack as pp
 from paper_2404_09529_amd import workloads as W
 
-from .gpu_util import bf16_dev, f32_dev, host64, i32_dev, report, require_gpu
+from .gpu_util import bf16_dev, f32_dev, gate_vs_floor, host64, i32_dev, report, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -136,8 +136,8 @@ def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
             want, floor = ref[i].logits[t], flo[i].logits[t]
             err = np.abs(lg[i] - want)
             ferr = np.abs(floor - want)
-            assert err.mean() <= 1.5 * ferr.mean() + 1e-4 and err.max() <= 2 * ferr.max() + 1e-3, \
-                (t, i, err.max(), err.mean(), ferr.max(), ferr.mean())
+            gate_vs_floor(f"{model_name} step {t} prompt {i} logits", [(err.max(), err.mean())],
+                          [(ferr.max(), ferr.mean())])
             slack = 2 * err.max()
             top = np.sort(want)[::-1]
             if top[0] - top[1] > slack:
@@ -157,7 +157,7 @@ def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
             fm, fa = max(e[2] for e in errs), np.mean([e[3] for e in errs])
             print(f"[parity] {model_name} generated {which}{l}: max {gm:.3e} mean {ga:.3e} "
                   f"(bf16 floor {fm:.3e} / {fa:.3e})", flush=True)
-            assert ga <= 1.5 * fa + 1e-4 and gm <= 2 * fm + 1e-3
+            gate_vs_floor(f"{model_name} generated {which}{l}", [(gm, ga)], [(fm, fa)])
 
 
 # ----------------------------------------------------------------------------- layouts and entry points agree
