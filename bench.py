@@ -17,7 +17,10 @@ Prints one JSON line:
                    timed live with HIP events on its stream, against the bf16 MFMA peak;
                    `traffic` is its HBM bytes per launch from the committed counter summary,
                    reported only while the kernel source still matches the one measured
-  cpu_baseline     the CPU oracle timed on a bounded sample of the same workload
+  cpu_baseline     the CPU oracle (float32) timed on a stratified sample of the same batch that
+                   includes its longest prompt, extrapolated to the whole batch by FLOP
+  device_memory    workspace, outputs and peak device memory of packed and padded prefill
+  pack_ms          the pp_pack C call (plan arrays allocated once)
 
 --traffic-pass runs only that kernel and a plain copy of known size, for the hardware
 counter passes (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE) that calibrate and measure it.
@@ -33,8 +36,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
-PEAK_FP32_TFLOPS = 157.3    # MI355X published fp32 vector rate (packed FMA; with packed FP32 off,
-                            # as this library is built, one FMA per lane per clock caps it at 78.6)
+PEAK_FP32_TFLOPS = 78.6     # fp32 FMA on the vector ALUs: 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x
+                            # 2.4 GHz.  The published 157.3 counts packed FMAs (two per lane per
+                            # clock), which this library is built without.
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 METRIC = "effective prefill tokens/s + TFLOP/s (% bf16 MFMA peak) vs padded prefill"
 GEMM_SOURCE = os.path.join(ROOT, "paper_2404_09529_amd", "csrc", "k_gemm_bf16.hip")
@@ -74,6 +78,23 @@ def attention_pairs(plan, lengths, tiled=True, key_tile=64):
     n_kv = np.minimum(q0 + qt, n)
     exe = int((qt * key_tile * ((n_kv + key_tile - 1) // key_tile)).sum()) if tiled else alg
     return {"algorithmic": alg, "executed": exe, "inflation": round(exe / max(alg, 1), 3)}
+
+
+def prefill_memory(step, base_alloc):
+    """Device memory of one pp_prefill setup (workspace, hidden states, K/V caches) and the
+    peak allocated above what was resident before it (weights, tokens, plan), after one call."""
+    import torch
+    nb = lambda t: t.numel() * t.element_size()
+    return {"workspace_bytes": nb(step.workspace), "outputs_bytes": nb(step.hidden) + nb(step.k_cache) + nb(step.v_cache),
+            "extra_peak_bytes": int(torch.cuda.max_memory_allocated() - base_alloc),
+            "peak_alloc_bytes": int(torch.cuda.max_memory_allocated())}
+
+
+def model_bytes(model):
+    import torch
+    return int(sum(t.numel() * t.element_size() for t in vars(model).values() if isinstance(t, torch.Tensor)) +
+               sum(t.numel() * t.element_size() for layer in model.layers for t in layer.values()
+                   if isinstance(t, torch.Tensor)))
 
 
 def time_steps(fn, steps, warmup):
@@ -156,32 +177,87 @@ def traffic_pass(args):
           flush=True)
 
 
-def cpu_baseline(case, budget_s):
-    """The oracle (float64, per prompt, as it stands) on prompts of the workload taken in
-    original order, skipping prompts longer than 512 tokens, until budget_s has elapsed."""
-    import numpy as np
-    from oracle import decoder as D
+def cpu_model():
     try:
-        from threadpoolctl import threadpool_info
-        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:
-        cores = 1
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def prompt_flops(shape, l):
+    """Algorithmic FLOP of one prompt of l tokens through one decoder layer (as
+    algorithmic_flops, per layer)."""
+    s = shape
+    lin = 2 * (s.d_model * (s.n_heads + 2 * s.n_kv_heads) * s.head_dim + s.n_heads * s.head_dim * s.d_model
+               + 3 * s.d_model * s.ffn_dim)
+    return l * lin + 4 * s.n_heads * s.head_dim * (l * (l + 1) // 2)
+
+
+def cpu_baseline(case):
+    """The oracle as it stands (per prompt, numpy), in float32, on the host's cores, over a
+    stratified sample of the batch, extrapolated to the whole batch by algorithmic FLOP.
+
+    The prompts are split by length into four quartiles; from each the prompt of median
+    length is timed, and from the top quartile also the batch's longest prompt.  Each is
+    timed through one decoder layer (the oracle's per-layer work is the same in every
+    layer, so n layers take n times as long); a quartile's time is its sampled prompts' time
+    scaled by the quartile's FLOP over theirs.  The embedding and final norm are left out
+    (no FLOP)."""
+    import dataclasses
+
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import decoder as D
+    affinity = len(os.sched_getaffinity(0))
+    threads = int(os.environ.get("OMP_NUM_THREADS", affinity) or affinity)
+    threads = max(1, min(threads, affinity))
     shape = D.Shape.of(case.shape)
-    off = np.concatenate([[0], np.cumsum(case.lengths)])
-    done, t0, used = 0, time.perf_counter(), []
-    for i, l in enumerate(case.lengths):
-        if l > 512:
-            continue
-        D.prefill_prompt(case.tokens[off[i]:off[i + 1]], case.weights, shape)
-        done += int(l)
-        used.append(i)
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    el = time.perf_counter() - t0
-    return {"value": done / el, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{len(used)} prompts ({done} tokens) of the same batch in original order, prompts "
-                      f"longer than 512 tokens skipped; float64 numpy oracle, all {shape.n_layers} layers; "
-                      f"{el:.1f} s"}
+    one = dataclasses.replace(shape, n_layers=1)
+    lengths = np.asarray(case.lengths, dtype=np.int64)
+    off = np.concatenate([[0], np.cumsum(lengths)])
+    order = np.argsort(lengths, kind="stable")
+    strata = [q for q in np.array_split(order, 4) if len(q)]
+    longest = int(order[-1])
+    total_s, timed, t_all = 0.0, [], time.perf_counter()
+    with threadpool_limits(limits=threads):
+        D.prefill_prompt(case.tokens[off[0]:off[0] + min(16, int(lengths[0]))], case.weights, one,
+                         dtype=np.float32)                      # warm-up
+        for qi, q in enumerate(strata):
+            picks = [int(q[len(q) // 2])]
+            if qi == len(strata) - 1 and longest not in picks:
+                picks.append(longest)
+            t = time.perf_counter()
+            for i in picks:
+                D.prefill_prompt(case.tokens[off[i]:off[i + 1]], case.weights, one, dtype=np.float32)
+            el = time.perf_counter() - t
+            f_sample = sum(prompt_flops(shape, int(lengths[i])) for i in picks)
+            f_stratum = sum(prompt_flops(shape, int(lengths[i])) for i in q)
+            total_s += el * f_stratum / f_sample * shape.n_layers
+            timed += [(int(i), int(lengths[i])) for i in picks]
+    wall = time.perf_counter() - t_all
+    L = int(lengths.sum())
+    return {"value": L / total_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "affinity_cpus": affinity, "dtype": "f32",
+            "extrapolated_batch_s": round(total_s, 2),
+            "sample": f"stratified: the median-length prompt of each length quartile plus the longest prompt, "
+                      f"{len(timed)} prompts (ids, lengths) {timed}, each through 1 of the {shape.n_layers} "
+                      f"layers; whole batch ({len(lengths)} prompts, {L} tokens, {shape.n_layers} layers) "
+                      f"extrapolated by algorithmic FLOP per quartile; float32 numpy oracle on {threads} "
+                      f"threads; {wall:.1f} s timed"}
+
+
+def gemm_rows_executed(plan, bm=256):
+    """Rows of the packed batch the projection GEMMs compute: every 256-row tile holding a real
+    slot (tiles of row-tail padding alone are skipped)."""
+    import numpy as np
+    real = np.asarray(plan.slot_kv) >= 0
+    T = plan.n_slots
+    return int(sum(min(bm, T - m0) for m0 in range(0, T, bm) if real[m0:m0 + bm].any()))
 
 
 # ----------------------------------------------------------------------------- sweeps
@@ -512,7 +588,6 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-padded", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--kernel-launches", type=int, default=20)
     ap.add_argument("--traffic-pass", action="store_true",
                     help="run only the dominant kernel and the calibration copy (for counter passes)")
@@ -572,12 +647,20 @@ def main():
     log(f"workload {case.wl.name}: k={len(lengths)} L={case.total_len} m={lengths.max()} "
         f"(weights drawn in {time.perf_counter() - t:.1f} s)")
 
-    # host planning, timed on its own
+    # host planning, timed on its own: the C call into plan arrays allocated once, and the
+    # binding's pp_pack (which allocates the arrays and copies them out) for reference
     n_pack = 50
+    bufs = pp.PlanBuffers(len(lengths), case.capacity)
+    l32 = np.ascontiguousarray(lengths, dtype=np.int32)
+    bufs.pack(l32, case.capacity)
+    t = time.perf_counter()
+    for _ in range(n_pack):
+        bufs.pack(l32, case.capacity)
+    pack_ms = (time.perf_counter() - t) * 1e3 / n_pack
     t = time.perf_counter()
     for _ in range(n_pack):
         plan = pp.pp_pack(lengths, case.capacity)
-    pack_ms = (time.perf_counter() - t) * 1e3 / n_pack
+    pack_binding_ms = (time.perf_counter() - t) * 1e3 / n_pack
     dplan = pp.DevicePlan(plan)          # first device allocations: allocator start-up, untimed
     torch.cuda.synchronize()
     n_up = 10
@@ -588,7 +671,13 @@ def main():
     upload_ms = (time.perf_counter() - t) * 1e3 / n_up
     model = pp.DeviceModel(shape, case.weights)
     tokens = torch.from_numpy(case.tokens).cuda()
+    torch.cuda.synchronize()
+    base_alloc = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
     step = pp.Prefill(model, dplan)
+    step(tokens)
+    torch.cuda.synchronize()
+    mem_packed = prefill_memory(step, base_alloc)
     log(f"packed plan: {plan.n_rows} rows x {plan.capacity}, fill {case.total_len / plan.n_slots:.3f}, "
         f"pack {pack_ms:.3f} ms, upload {upload_ms:.2f} ms")
 
@@ -638,7 +727,10 @@ def main():
         "algorithmic_flop": flops,
         "ms_median": round(packed["ms_median"], 4), "ms_p10": round(packed["ms_p10"], 4),
         "ms_p90": round(packed["ms_p90"], 4),
-        "pack_ms": round(pack_ms, 4), "plan_upload_ms": round(upload_ms, 3),
+        "pack_ms": round(pack_ms, 4), "pack_binding_ms": round(pack_binding_ms, 4),
+        "plan_upload_ms": round(upload_ms, 3),
+        "gemm_rows_executed_over_L": round(gemm_rows_executed(plan) / case.total_len, 4),
+        "device_memory": {"packed": mem_packed, "weights_bytes": model_bytes(model)},
         "attention_pairs": attention_pairs(plan, lengths, tiled=bf),
         "roofline": {"kernel": k_name, "bound": "mfma" if bf else "alu",
                      "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
@@ -673,7 +765,16 @@ def main():
 
     if not args.no_padded:
         pplan = pp.pp_pack_padded(lengths)
-        pstep = pp.Prefill(model, pp.DevicePlan(pplan))
+        pdplan = pp.DevicePlan(pplan)
+        torch.cuda.synchronize()
+        base_alloc = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        pstep = pp.Prefill(model, pdplan)
+        pstep(tokens)
+        torch.cuda.synchronize()
+        out["device_memory"]["padded"] = prefill_memory(pstep, base_alloc)
+        out["device_memory"]["padded_over_packed"] = round(
+            out["device_memory"]["padded"]["extra_peak_bytes"] / out["device_memory"]["packed"]["extra_peak_bytes"], 3)
         padded = time_steps(lambda: pstep(tokens), max(3, args.steps // 4), 1)
         pms = padded["ms_mean"]
         out["padded"] = {"ms_per_step": round(pms, 4), "tokens_per_s": round(case.total_len / (pms / 1e3), 1),
@@ -686,8 +787,9 @@ def main():
         torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(case, args.cpu_budget_s)
-        log(f"cpu oracle: {out['cpu_baseline']['value']:.1f} tokens/s on {out['cpu_baseline']['cores']} threads")
+        out["cpu_baseline"] = cpu_baseline(case)
+        log(f"cpu oracle: {out['cpu_baseline']['value']:.1f} tokens/s on {out['cpu_baseline']['cores']} threads "
+            f"({out['cpu_baseline']['cpu_model']})")
 
     if args.calibration_copy:
         calibration_copy()

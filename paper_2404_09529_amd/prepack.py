@@ -205,6 +205,27 @@ def _run_pack(lengths: Sequence[int], capacity: Optional[int], slot_cap=None, qt
                 qtile_seg=arrs["qtile_seg"][: p.n_qtiles].copy(), qtile_q0=arrs["qtile_q0"][: p.n_qtiles].copy())
 
 
+class PlanBuffers:
+    """Host arrays for plans of up to k prompts in rows of up to C slots, allocated once, so
+    that packing batch after batch costs only the C call (``pack`` returns the filled pp_plan
+    struct; its arrays stay valid until the next call)."""
+
+    def __init__(self, k: int, C: int):
+        bs, bq = pp_plan_bounds(k, C)
+        self.k = k
+        self.arrs = {n: np.empty(max(size, 1), dtype=np.int32) for n, size in
+                     [("row_seg_ptr", k + 1), ("seg_prompt", k), ("seg_start", k), ("seg_len", k),
+                      ("prompt_kv_off", k + 1), ("slot_seg", bs), ("slot_pos", bs), ("slot_kv", bs),
+                      ("qtile_seg", bq), ("qtile_q0", bq)]}
+        self.struct = PPPlan(slot_cap=bs, qtile_cap=bq, **{n: _ptr(a) for n, a in self.arrs.items()})
+
+    def pack(self, lengths: np.ndarray, capacity: int) -> PPPlan:
+        """pp_pack of int32 contiguous ``lengths`` (at most k of them, rows of at most C)."""
+        _check(lib().pp_pack(_ptr(lengths), int(lengths.size), int(capacity), ctypes.byref(self.struct)),
+               "pp_pack")
+        return self.struct
+
+
 def pp_pack(lengths: Sequence[int], capacity: int = 0, **caps) -> Plan:
     """First-fit-decreasing packing into rows of ``capacity`` slots (0 = max length)."""
     return _run_pack(lengths, capacity, **caps)
