@@ -12,7 +12,8 @@
  *     a message for the calling thread available from pp_last_error();
  *   - no exception, abort or exit crosses the ABI;
  *   - the library allocates nothing and keeps no state between calls: every
- *     buffer, host or device, belongs to the caller;
+ *     buffer, host or device, belongs to the caller (one exception: the static
+ *     device buffer behind pp_first_token_noalloc);
  *   - "device pointer" means memory of the current HIP device; "host pointer"
  *     means ordinary process memory.
  */
@@ -306,6 +307,32 @@ pp_status pp_first_token_workspace_size(const pp_config* cfg, const pp_dplan* pl
  *         PP_ERR_HIP (launch failure). */
 pp_status pp_first_token(const pp_config* cfg, const pp_dplan* plan, const float* hidden, const void* lm_head,
                          void* workspace, size_t workspace_bytes, float* logits, int32_t* tokens, void* stream);
+
+/* Bytes of the library-owned device buffer behind pp_first_token_noalloc (per GPU). */
+#define PP_FIRST_TOKEN_SCRATCH_BYTES (16u << 20)
+
+/* pp_first_token for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same kernels and the
+ * same results, with the workspace taken from a static device buffer of
+ * PP_FIRST_TOKEN_SCRATCH_BYTES that the library holds on every GPU it runs on until the
+ * process ends.  The call allocates nothing (no hipMalloc, no hipFree); the caller still
+ * passes hidden, lm_head, logits and tokens.
+ *
+ *   Limit: pp_first_token_workspace_size(cfg, plan) <= PP_FIRST_TOKEN_SCRATCH_BYTES, else
+ *          PP_ERR_BUFFER_TOO_SMALL before anything is enqueued.  bf16 needs about
+ *          k (2 d + 8 vocab / 128) bytes: e.g. 512 prompts at d = 8192 with a 128,256-token
+ *          vocabulary; float32 about k (4 d + 8 vocab): e.g. 64 prompts with vocab 32,000
+ *          do not fit.
+ *   Sharing: every call on a GPU uses that GPU's one buffer; calls that overlap on one GPU
+ *          (concurrent streams, or threads with the same device) race on it and must be
+ *          serialised by the caller.  No part of the buffer needs to start at any value:
+ *          every byte a call reads was written earlier in the same call.
+ *   Set-up: the first call on a device looks up that device's buffer address (no allocation,
+ *          no stream work); a caller that captures a graph can make one call before capture.
+ * Errors: as pp_first_token, with PP_ERR_BUFFER_TOO_SMALL for the limit above and PP_ERR_HIP
+ *         when the buffer's address cannot be obtained. */
+pp_status pp_first_token_noalloc(const pp_config* cfg, const pp_dplan* plan, const float* hidden,
+                                 const void* lm_head, float* logits, int32_t* tokens, void* stream);
 
 /* ------------------------------------------------------------------------------------------
  * Generation with packed KV caches (section 4.8: the caches of a batch are packed for

@@ -12,6 +12,9 @@
 // per-workgroup pairs; the order it uses is total, so the result is deterministic.
 #include <math.h>
 
+#include <mutex>
+#include <vector>
+
 #include "device.h"
 #include "kernels.h"
 #include "prepack.h"
@@ -236,7 +239,31 @@ __global__ __launch_bounds__(256) void argmax_finalize_kernel(const ArgMax* __re
 
 }  // namespace
 
+// Workspace of pp_first_token_noalloc: a file-scope array of this code object, one copy per
+// GPU, alive until the process ends.  In host code its name is only a stand-in for the device
+// symbol: host code passes kernels the device address that hipGetSymbolAddress returns for
+// the current GPU (first_token_scratch), never the array itself.
+static __device__ __align__(256) char scratch[PP_FIRST_TOKEN_SCRATCH_BYTES];
+
 namespace ppk {
+
+hipError_t first_token_scratch(void** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    static std::mutex mu;
+    static std::vector<void*> by_device;     // device id -> address of its copy of `scratch`
+    std::lock_guard<std::mutex> lock(mu);
+    if (dev >= static_cast<int>(by_device.size())) by_device.resize(dev + 1, nullptr);
+    if (!by_device[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        by_device[dev] = p;
+    }
+    *ptr = by_device[dev];
+    return hipSuccess;
+}
 
 size_t first_token_workspace(int dtype, int k, int V, int d) {
     const int k_pad = (k + 15) / 16 * 16;

@@ -91,6 +91,9 @@ void attention_f32(const float* q, int64_t ldq, const float* kc, const float* vc
 size_t first_token_workspace(int dtype, int k, int V, int d);
 void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, int k, const void* lm_head, int V,
                  int d, void* workspace, float* logits, int32_t* tokens, hipStream_t s);
+// The current GPU's copy of the static PP_FIRST_TOKEN_SCRATCH_BYTES workspace of
+// pp_first_token_noalloc (its address looked up once per device).
+hipError_t first_token_scratch(void** ptr);
 
 // ---------------------------------------------------------------------- generation (decode)
 constexpr int kDecodeChunk = 128;   // keys per workgroup of the decode attention

@@ -408,24 +408,60 @@ extern "C" pp_status pp_first_token_workspace_size(const pp_config* cfg, const p
     return PP_OK;
 }
 
-extern "C" pp_status pp_first_token(const pp_config* cfg, const pp_dplan* plan, const float* hidden,
-                                    const void* lm_head, void* workspace, size_t workspace_bytes, float* logits,
-                                    int32_t* tokens, void* stream) {
-    pp::clear_error();
+namespace {
+
+// The checks pp_first_token and pp_first_token_noalloc share; *need = workspace bytes.
+pp_status check_first_token(const pp_config* cfg, const pp_dplan* plan, const float* hidden, const void* lm_head,
+                            const int32_t* tokens, size_t* need) {
     if (pp_status st = validate_config(cfg)) return st;
     if (pp_status st = validate_plan(plan)) return st;
+    *need = 0;
     if (plan->k == 0) return PP_OK;
     if (plan->total_len < plan->k)
         return pp::fail(PP_ERR_INVALID_ARG, "plan has %d prompts but %d tokens", plan->k, plan->total_len);
     if (!plan->prompt_kv_off) return pp::fail(PP_ERR_INVALID_ARG, "prompt_kv_off is NULL");
-    if (!hidden || !lm_head || !tokens || !workspace) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
+    if (!hidden || !lm_head || !tokens) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
+    *need = ppk::first_token_workspace(cfg->dtype, plan->k, cfg->vocab, cfg->d_model);
+    return PP_OK;
+}
+
+}  // namespace
+
+extern "C" pp_status pp_first_token(const pp_config* cfg, const pp_dplan* plan, const float* hidden,
+                                    const void* lm_head, void* workspace, size_t workspace_bytes, float* logits,
+                                    int32_t* tokens, void* stream) {
+    pp::clear_error();
+    size_t need = 0;
+    if (pp_status st = check_first_token(cfg, plan, hidden, lm_head, tokens, &need)) return st;
+    if (plan->k == 0) return PP_OK;
+    if (!workspace) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
         return pp::fail(PP_ERR_INVALID_ARG, "workspace is not %zu-byte aligned", kAlign);
-    const size_t need = ppk::first_token_workspace(cfg->dtype, plan->k, cfg->vocab, cfg->d_model);
     if (workspace_bytes < need)
         return pp::fail(PP_ERR_BUFFER_TOO_SMALL, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
     (void)hipGetLastError();
     ppk::first_token(cfg->dtype, hidden, plan->prompt_kv_off, plan->k, lm_head, cfg->vocab, cfg->d_model, workspace,
                      logits, tokens, static_cast<hipStream_t>(stream));
     return finish("first_token");
+}
+
+extern "C" pp_status pp_first_token_noalloc(const pp_config* cfg, const pp_dplan* plan, const float* hidden,
+                                            const void* lm_head, float* logits, int32_t* tokens, void* stream) {
+    pp::clear_error();
+    size_t need = 0;
+    if (pp_status st = check_first_token(cfg, plan, hidden, lm_head, tokens, &need)) return st;
+    if (plan->k == 0) return PP_OK;
+    if (need > PP_FIRST_TOKEN_SCRATCH_BYTES)
+        return pp::fail(PP_ERR_BUFFER_TOO_SMALL,
+                        "%d prompts with vocab %d and d %d need %zu bytes of workspace, more than the %u bytes "
+                        "of pp_first_token_noalloc's static buffer (use pp_first_token)",
+                        plan->k, cfg->vocab, cfg->d_model, need, PP_FIRST_TOKEN_SCRATCH_BYTES);
+    void* ws = nullptr;
+    const hipError_t e = ppk::first_token_scratch(&ws);
+    if (e != hipSuccess)
+        return pp::fail(PP_ERR_HIP, "address of the static first-token buffer: %s", hipGetErrorString(e));
+    (void)hipGetLastError();
+    ppk::first_token(cfg->dtype, hidden, plan->prompt_kv_off, plan->k, lm_head, cfg->vocab, cfg->d_model, ws, logits,
+                     tokens, static_cast<hipStream_t>(stream));
+    return finish("first_token_noalloc");
 }

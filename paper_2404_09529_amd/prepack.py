@@ -114,6 +114,7 @@ def lib() -> ctypes.CDLL:
         L.pp_final_norm_unpack.argtypes = [vp, vp, i32, f32, dpp, vp, vp]
         L.pp_first_token_workspace_size.argtypes = [cfgp, dpp, ctypes.POINTER(ctypes.c_size_t)]
         L.pp_first_token.argtypes = [cfgp, dpp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp]
+        L.pp_first_token_noalloc.argtypes = [cfgp, dpp, vp, vp, vp, vp, vp]
         glp, gdp, wp = ctypes.POINTER(PPGenLayout), ctypes.POINTER(PPGenDLayout), ctypes.POINTER(PPWeights)
         L.pp_gen_layout_make.argtypes = [_i32p, i32, i32, i32, glp]
         L.pp_decode_workspace_size.argtypes = [cfgp, gdp, ctypes.POINTER(ctypes.c_size_t)]
@@ -122,6 +123,7 @@ def lib() -> ctypes.CDLL:
         for name in ("pp_plan_bounds", "pp_pack", "pp_pack_padded", "pp_prefill_workspace_size", "pp_prefill",
                      "pp_embed", "pp_rmsnorm", "pp_gemm", "pp_rope", "pp_kv_scatter", "pp_attention",
                      "pp_final_norm_unpack", "pp_first_token_workspace_size", "pp_first_token",
+                     "pp_first_token_noalloc",
                      "pp_gen_layout_make", "pp_decode_workspace_size", "pp_decode_step", "pp_generate"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -413,6 +415,16 @@ def pp_first_token(cfg: PPConfig, dplan: DevicePlan, hidden, lm_head, workspace,
                                 _p(workspace), workspace.numel() * workspace.element_size(), _p(logits),
                                 _p(tokens), _stream(stream)), "pp_first_token")
 
+
+
+PP_FIRST_TOKEN_SCRATCH_BYTES = 16 << 20
+
+
+def pp_first_token_noalloc(cfg: PPConfig, dplan: DevicePlan, hidden, lm_head, tokens, logits=None,
+                           stream=None) -> None:
+    """pp_first_token with the library's static device workspace (allocates nothing)."""
+    _check(lib().pp_first_token_noalloc(ctypes.byref(cfg), ctypes.byref(dplan.struct), _p(hidden), _p(lm_head),
+                                        _p(logits), _p(tokens), _stream(stream)), "pp_first_token_noalloc")
 
 
 # ----------------------------------------------------------------------------- generation

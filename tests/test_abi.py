@@ -275,6 +275,31 @@ def test_first_token_workspace_and_rejections(L):
     assert call(p=_dplan(k=0, total_len=0)) == pp.PP_OK            # no prompt: nothing to do
 
 
+def test_first_token_noalloc_rejections(L):
+    """The allocation-free first token: the same argument checks, and a plan whose workspace
+    exceeds the static buffer rejected before anything is enqueued (no GPU touched)."""
+    f = L.pp_first_token_noalloc
+    cfg, dp = _cfg(vocab=32000), _dplan()
+    def call(c=cfg, p=dp, h=0x1000, w=0x2000, tok=0x3000):
+        return f(ctypes.byref(c), ctypes.byref(p), h, w, None, tok, None)
+    assert call(h=None) == pp.PP_ERR_INVALID_ARG
+    assert call(w=None) == pp.PP_ERR_INVALID_ARG
+    assert call(tok=None) == pp.PP_ERR_INVALID_ARG
+    assert call(p=_dplan(total_len=1)) == pp.PP_ERR_INVALID_ARG
+    assert call(p=_dplan(k=0, total_len=0)) == pp.PP_OK
+    # float32 keeps one (value, id) pair per vocabulary row and prompt: 2,000,000 x 2 x 8 bytes
+    big = _cfg(dtype=pp.PP_F32, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=688, vocab=2_000_000)
+    n = ctypes.c_size_t()
+    assert L.pp_first_token_workspace_size(ctypes.byref(big), ctypes.byref(dp), ctypes.byref(n)) == pp.PP_OK
+    assert n.value > pp.PP_FIRST_TOKEN_SCRATCH_BYTES
+    assert call(c=big) == pp.PP_ERR_BUFFER_TOO_SMALL
+    assert "static buffer" in pp.pp_last_error()
+    # a header constant the binding mirrors
+    text = open(os.path.join(ROOT, "include", "prepack.h")).read()
+    assert re.search(r"#define PP_FIRST_TOKEN_SCRATCH_BYTES \(16u << 20\)", text)
+    assert pp.PP_FIRST_TOKEN_SCRATCH_BYTES == 16 << 20
+
+
 # ----------------------------------------------------------------------------- generation
 def test_gen_layout_packed_and_padded_by_hand(L):
     """pp_gen_layout_make on lengths 3, 1, 5 with room for 4 new tokens."""
