@@ -251,13 +251,13 @@ def cpu_baseline(case):
                       f"threads; {wall:.1f} s timed"}
 
 
-def gemm_rows_executed(plan, bm=256):
-    """Rows of the packed batch the projection GEMMs compute: every 256-row tile holding a real
-    slot (tiles of row-tail padding alone are skipped)."""
-    import numpy as np
-    real = np.asarray(plan.slot_kv) >= 0
+def gemm_rows_executed(plan):
+    """Rows of the packed batch the projection GEMMs compute: the plan's row tiles (every
+    PP_MTILE-slot tile holding a slot of some span; tiles of row-tail padding alone are
+    skipped)."""
+    from paper_2404_09529_amd import prepack as pp
     T = plan.n_slots
-    return int(sum(min(bm, T - m0) for m0 in range(0, T, bm) if real[m0:m0 + bm].any()))
+    return int(sum(min(pp.PP_MTILE, T - int(m0)) for m0 in plan.mtile_m0))
 
 
 # ----------------------------------------------------------------------------- sweeps

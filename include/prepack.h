@@ -41,6 +41,9 @@ typedef enum pp_dtype { PP_F32 = 0, PP_BF16 = 1 } pp_dtype;
 /* Query-tile length of the attention work list carried in a plan. */
 #define PP_QTILE 128
 
+/* Row-tile length (slots) of the projection GEMMs' tile list carried in a plan. */
+#define PP_MTILE 256
+
 /* Text for the last non-OK status returned on the calling thread ("" if none). */
 const char* pp_last_error(void);
 
@@ -70,8 +73,13 @@ const char* pp_version(void);
  *   qtile_q0      [qtile_cap] first query (offset inside the segment) of each query tile;
  *                             every (segment, multiple of PP_QTILE below seg_len) appears
  *                             once, tiles with more keys to visit first
- * slot_cap must be >= k * C and qtile_cap >= k * ceil(C / PP_QTILE), where C is the
- * row capacity actually used (pp_plan_bounds computes both).
+ *   mtile_m0      [mtile_cap] row tiles of the projection GEMMs: the first slot of every
+ *                             PP_MTILE-slot tile of the batch (slots t0 .. t0 + PP_MTILE - 1,
+ *                             t0 a multiple of PP_MTILE) holding a slot of some span,
+ *                             ascending; tiles of row-tail padding alone are left out
+ * slot_cap must be >= k * C, qtile_cap >= k * ceil(C / PP_QTILE) and mtile_cap >=
+ * ceil(k * C / PP_MTILE), where C is the row capacity actually used (pp_plan_bounds computes
+ * all three).
  * ---------------------------------------------------------------------------------------- */
 typedef struct pp_plan {
     /* written by pp_pack / pp_pack_padded */
@@ -81,9 +89,11 @@ typedef struct pp_plan {
     int32_t max_len;    /* m = max l_i                                               */
     int32_t total_len;  /* L = sum l_i                                               */
     int32_t n_qtiles;   /* entries written to qtile_seg / qtile_q0                   */
+    int32_t n_mtiles;   /* entries written to mtile_m0                               */
     /* set by the caller */
     int64_t slot_cap;
     int64_t qtile_cap;
+    int64_t mtile_cap;
     int32_t* row_seg_ptr;
     int32_t* seg_prompt;
     int32_t* seg_start;
@@ -94,11 +104,12 @@ typedef struct pp_plan {
     int32_t* slot_kv;
     int32_t* qtile_seg;
     int32_t* qtile_q0;
+    int32_t* mtile_m0;
 } pp_plan;
 
 /* Array sizes a plan needs for k prompts in rows of C slots (C = capacity, or the maximum
  * length when capacity is 0 or the plan is padded).  Errors: k < 0, C < 0, NULL outputs. */
-pp_status pp_plan_bounds(int32_t k, int32_t C, int64_t* slot_cap, int64_t* qtile_cap);
+pp_status pp_plan_bounds(int32_t k, int32_t C, int64_t* slot_cap, int64_t* qtile_cap, int64_t* mtile_cap);
 
 /* BINPACK + TENSORIZE layout + RESTART-PE + UNPACK map (Algorithm 1; sections 3.1-3.2).
  *
@@ -111,7 +122,7 @@ pp_status pp_plan_bounds(int32_t k, int32_t C, int64_t* slot_cap, int64_t* qtile
  * lengths: host [k], every l_i >= 1.  k == 0 is valid and yields an empty plan.
  * Errors: PP_ERR_INVALID_ARG (NULL, k < 0, l_i <= 0, capacity < 0),
  *         PP_ERR_TOO_LONG (some l_i > capacity > 0),
- *         PP_ERR_BUFFER_TOO_SMALL (slot_cap / qtile_cap below pp_plan_bounds).
+ *         PP_ERR_BUFFER_TOO_SMALL (slot_cap / qtile_cap / mtile_cap below pp_plan_bounds).
  * Pure host code, reentrant, O(k log k + k r + r C). */
 pp_status pp_pack(const int32_t* lengths, int32_t k, int32_t capacity, pp_plan* plan);
 
@@ -164,9 +175,9 @@ typedef struct pp_weights {
 
 /* A plan copied to device memory: the scalars of pp_plan and device copies of the arrays
  * the kernels read (same meaning and length as in pp_plan; slot arrays hold
- * n_rows * capacity entries, qtile arrays n_qtiles). */
+ * n_rows * capacity entries, qtile arrays n_qtiles, mtile_m0 n_mtiles). */
 typedef struct pp_dplan {
-    int32_t k, capacity, n_rows, max_len, total_len, n_qtiles;
+    int32_t k, capacity, n_rows, max_len, total_len, n_qtiles, n_mtiles;
     const int32_t* seg_prompt;
     const int32_t* seg_start;
     const int32_t* seg_len;
@@ -176,6 +187,7 @@ typedef struct pp_dplan {
     const int32_t* slot_kv;
     const int32_t* qtile_seg;
     const int32_t* qtile_q0;
+    const int32_t* mtile_m0;
 } pp_dplan;
 
 /* Bytes of device workspace pp_prefill needs for this config and plan.
@@ -237,8 +249,8 @@ pp_status pp_rmsnorm(int32_t dtype, const float* x, const float* gain, int32_t r
 /* Projection GEMM C = A B^T: A [M, K] (row stride lda), B [N, K] (row stride ldb), both dtype,
  * float32 accumulation; C per epilogue (row stride ldc).  bf16: N % 256 == 0, K % 64 == 0;
  * f32: K % 16 == 0 and no PP_EPI_SWIGLU.  plan may be NULL; when given (bf16 only, and then
- * M must be n_rows * capacity), row tiles made only of row-tail padding are skipped, as in
- * pp_prefill, and their rows of C are left unwritten. */
+ * M must be n_rows * capacity), only the plan's row tiles (mtile_m0) are computed, as in
+ * pp_prefill: rows of C in tiles of row-tail padding alone are left unwritten. */
 pp_status pp_gemm(int32_t dtype, int32_t epilogue, const void* A, int64_t lda, const void* B, int64_t ldb,
                   void* C, int64_t ldc, int32_t M, int32_t N, int32_t K, const pp_dplan* plan, void* stream);
 

@@ -193,7 +193,7 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
             pending = ppk::skinny_split(d, hd).splits;
         } else if (bf) {
             const ppk::QkvOut qo{q, hd, gk, gv, kvw, table, slot_pos, slot_kv, H, Hkv};
-            ppk::qkv_rope_bf16(xn, d, w->wqkv[l], d, k, d, slot_seg, k, qo, s);
+            ppk::qkv_rope_bf16(xn, d, w->wqkv[l], d, k, d, nullptr, 0, qo, s);
             ppk::decode_attention(dt, q, hd, ck, cv, gk, gv, kvw, Ly, step, H, Hkv, D, part, attn, hd, s);
             ppk::gemm_bf16(ppk::kResidual, attn, hd, w->wo[l], hd, x, d, k, d, hd, nullptr, 0, s);
         } else {

@@ -33,9 +33,10 @@
 // round-robin, so XCD x runs workgroups x, x + 8, ...; each XCD owns a contiguous block of
 // M-tiles ordered in groups of up to 8 M-tiles sweeping N, and its workgroups take that list
 // in strides of their count, so the 32 tiles resident on an XCD always form one compact
-// block, and the tiles sharing an A or B panel read it from the same L2.  M-tiles made
-// only of row-tail padding are skipped (packed batches only carry pads at row tails,
-// section 3.1).
+// block, and the tiles sharing an A or B panel read it from the same L2.  The M-tiles are
+// the plan's row-tile list: tiles made only of row-tail padding (packed batches carry pads
+// only at row tails, section 3.1) are not in it, so they are neither computed nor counted
+// when the tiles are split across the XCDs.
 #include "device.h"
 #include "kernels.h"
 
@@ -68,13 +69,6 @@ constexpr int kRsrcWord3 = 0x00020000;
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) & 1) | (((r >> 3) & 1) << 1) | (r & 4); }
 
 typedef __attribute__((address_space(3))) void lds_void;
-
-__device__ __forceinline__ bool tile_active(const int32_t* slot_seg, int capacity, int m0, int M) {
-    if (!slot_seg || slot_seg[m0] >= 0) return true;
-    // first slot is a row-tail pad: inactive unless another row starts inside the tile
-    const int64_t next_row = (int64_t(m0) / capacity + 1) * capacity;
-    return next_row < min(m0 + BM, M);
-}
 
 __device__ __forceinline__ void barrier() {
     __builtin_amdgcn_sched_barrier(0);
@@ -111,8 +105,7 @@ __device__ __forceinline__ void stage_put(char* stg, int r, int c, int half, bf1
 // of the epilogue.
 template <int EPI>
 __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ Cv, int64_t ldc, int M,
-                                         int mb, int nb0, int lane, const int32_t* __restrict__ slot_seg,
-                                         const ppk::QkvOut& qo, char* stg) {
+                                         int mb, int nb0, int lane, const ppk::QkvOut& qo, char* stg) {
     const int lr = lane & 15, g = lane >> 4;
     if constexpr (EPI == ppk::kResidual) {
         // C[m][nb0 ..] += this lane's accumulators, one 16-row block j at a time, staged
@@ -174,19 +167,18 @@ __device__ __forceinline__ void epilogue(f32x4 (&acc)[8][8], void* __restrict__ 
         // and the rotate-half partners c and c + 64 are accumulator blocks i and i + 4 of the
         // same lane: RoPE is applied to the float32 accumulators before the one rounding.
         // One 16-row block j at a time, staged through LDS (16 rows x 256 bytes) and stored
-        // as whole rows.  The slot metadata of all 8 of the lane's rows is read first; the
-        // cos/sin rows of block j + 1 are requested before block j is stored (vmcnt counts
-        // stores and completes in order).
+        // as whole rows.  The slot metadata of all 8 of the lane's rows is read first (a slot
+        // outside every span has position 0 and no cache row); the cos/sin rows of block j + 1
+        // are requested before block j is stored (vmcnt counts stores and completes in order).
         const int head = nb0 >> 7;
         const int kind = head < qo.H ? 0 : (head < qo.H + qo.Hkv ? 1 : 2);   // q, k, v (uniform)
         int drow[8], pos[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int m = mb + 16 * j + lr, mc = min(m, M - 1);
-            const int seg = slot_seg[mc], p = qo.slot_pos[mc];
             const int kv = kind > 0 ? qo.slot_kv[mc] : m;
             drow[j] = m < M ? kv : -1;
-            pos[j] = seg >= 0 ? p : 0;
+            pos[j] = qo.slot_pos[mc];
         }
         f32x4 tb[2][8];
         auto load_tab = [&](int j, f32x4 (&t)[8]) {
@@ -306,13 +298,15 @@ template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict__ A, int64_t lda,
                                                           const bf16* __restrict__ B, int64_t ldb,
                                                           void* __restrict__ Cv, int64_t ldc, int M, int K,
-                                                          const int32_t* __restrict__ slot_seg, int capacity,
-                                                          int tiles_m, int tiles_n, int balanced, ppk::QkvOut qo) {
+                                                          const int32_t* __restrict__ mtile_m0, int tiles_m,
+                                                          int tiles_n, int balanced, ppk::QkvOut qo) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases and descriptors in SGPRs
 
-    // ---- persistent schedule.  Workgroups are dealt to the 8 XCDs round-robin (XCD = id % 8)
+    // ---- persistent schedule over tiles_m M-tiles (M-tile i starts at row mtile_m0[i], or at
+    // row BM i without a list) and tiles_n N-tiles.  Workgroups are dealt to the 8 XCDs
+    // round-robin (XCD = id % 8)
     // and the grid holds one workgroup per CU, so XCD x runs workgroups x, x + 8, ... one per
     // CU.  XCD x owns the contiguous block of M-tiles [x pm, x pm + pm), ordered in groups of
     // at most 8 M-tiles, each group sweeping all N-tiles; its workgroups take that list in
@@ -347,19 +341,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
         const int gi = g_begin + local;
         const int group = gi / (gm * tiles_n), within = gi - group * gm * tiles_n;
         const int first = group * gm, gsz = min(m_cnt - first, gm);
-        return (m_begin + first + within % gsz) * BM;
+        const int mt = m_begin + first + within % gsz;
+        return mtile_m0 ? mtile_m0[mt] : mt * BM;
     };
     auto tile_n0 = [&](int local) {
         const int gi = g_begin + local;
         const int group = gi / (gm * tiles_n), within = gi - group * gm * tiles_n;
         const int first = group * gm, gsz = min(m_cnt - first, gm);
         return (within / gsz) * BN;
-    };
-    // the first tile of this workgroup's list at or after `local` that holds a real slot
-    auto next_active = [&](int local) {
-        for (; local < n_local; local += n_slots)
-            if (tile_active(slot_seg, capacity, tile_m0(local), M)) break;
-        return local;
     };
     const int nk = K / BK;
 
@@ -380,7 +369,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
     // load cursor: the K-step whose operand tiles are being requested, into slots l_sa (A)
     // and l_sb (B); l_local >= n_local once the stream is exhausted (its loads are then dead:
     // they read nothing and land in slots that are never read again)
-    int l_local = next_active(slot), l_kt = 0, l_sa = 0, l_sb = 1;
+    int l_local = slot, l_kt = 0, l_sa = 0, l_sb = 1;
     __amdgpu_buffer_rsrc_t rsrc_a, rsrc_b;
     const __amdgpu_buffer_rsrc_t rsrc_0 = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(A), 0, 0, kRsrcWord3);
     auto set_cursor_tile = [&]() {
@@ -414,7 +403,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
         if (l_local >= n_local) return;
         if (++l_kt == nk) {
             l_kt = 0;
-            l_local = next_active(l_local + n_slots);
+            l_local += n_slots;
             set_cursor_tile();
         }
     };
@@ -517,9 +506,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const bf16* __restrict
         // exactly the part of it that w's own loads refill.
         const int m0 = tile_m0(c_local), n0 = tile_n0(c_local);
         const int free_slot = c_sb >= 2 ? c_sb - 2 : c_sb + NSLOT - 2;
-        epilogue<EPI>(acc, Cv, ldc, M, m0 + wm * 128, n0 + wn * 128, lane, slot_seg, qo,
+        epilogue<EPI>(acc, Cv, ldc, M, m0 + wm * 128, n0 + wn * 128, lane, qo,
                       smem + free_slot * SLOT_B + wave * LOADS * 1024);
-        c_local = next_active(c_local + n_slots);
+        c_local += n_slots;
         if (c_local >= n_local) break;
     }
     __builtin_amdgcn_s_waitcnt(0);   // no load may still be writing LDS when the workgroup ends
@@ -535,14 +524,15 @@ constexpr size_t kLds = LDS_BYTES;
 
 template <int EPI>
 void launch(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc, int M, int N, int K,
-            const int32_t* slot_seg, int capacity, const QkvOut& qo, hipStream_t s) {
+            const int32_t* mtile_m0, int n_mtiles, const QkvOut& qo, hipStream_t s) {
     static bool attr = [] {
         (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI>),
                                   hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
         return true;
     }();
     (void)attr;
-    const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
+    const int tiles_m = mtile_m0 ? n_mtiles : (M + BM - 1) / BM, tiles_n = N / BN;
+    if (tiles_m <= 0) return;
     // one workgroup per CU (each needs the whole 160 KB LDS), a multiple of 8 so
     // that every XCD runs the same number; never more workgroups than tiles
     static const int n_cu = [] {
@@ -560,27 +550,26 @@ void launch(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int
     const int per_xcd = balanced ? even : blocked;
     const dim3 grid(8 * min(wg_per_xcd, per_xcd));
     gemm_bf16_kernel<EPI><<<grid, NT, kLds, s>>>(static_cast<const bf16*>(A), lda, static_cast<const bf16*>(B),
-                                                ldb, C, ldc, M, K, slot_seg, capacity, tiles_m, tiles_n, balanced,
-                                                qo);
+                                                ldb, C, ldc, M, K, mtile_m0, tiles_m, tiles_n, balanced, qo);
 }
 
 }  // namespace
 
 void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc, int M,
-               int N, int K, const int32_t* slot_seg, int capacity, hipStream_t s) {
+               int N, int K, const int32_t* mtile_m0, int n_mtiles, hipStream_t s) {
     if (M <= 0) return;
     const QkvOut none{};
     switch (epi) {
-        case kStore: launch<kStore>(A, lda, B, ldb, C, ldc, M, N, K, slot_seg, capacity, none, s); break;
-        case kResidual: launch<kResidual>(A, lda, B, ldb, C, ldc, M, N, K, slot_seg, capacity, none, s); break;
-        default: launch<kSwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, slot_seg, capacity, none, s); break;
+        case kStore: launch<kStore>(A, lda, B, ldb, C, ldc, M, N, K, mtile_m0, n_mtiles, none, s); break;
+        case kResidual: launch<kResidual>(A, lda, B, ldb, C, ldc, M, N, K, mtile_m0, n_mtiles, none, s); break;
+        default: launch<kSwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, mtile_m0, n_mtiles, none, s); break;
     }
 }
 
-void qkv_rope_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, int M, int K, const int32_t* slot_seg,
-                   int capacity, const QkvOut& out, hipStream_t s) {
+void qkv_rope_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, int M, int K, const int32_t* mtile_m0,
+                   int n_mtiles, const QkvOut& out, hipStream_t s) {
     if (M <= 0) return;
-    launch<kQkvRope>(A, lda, B, ldb, nullptr, 0, M, (out.H + 2 * out.Hkv) * 128, K, slot_seg, capacity, out, s);
+    launch<kQkvRope>(A, lda, B, ldb, nullptr, 0, M, (out.H + 2 * out.Hkv) * 128, K, mtile_m0, n_mtiles, out, s);
 }
 
 }  // namespace ppk

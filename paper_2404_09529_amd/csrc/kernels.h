@@ -39,7 +39,7 @@ enum Epilogue { kStore = 0, kResidual = 1, kSwiGLU = 2, kQkvRope = 3 };
 // Destinations of the kQkvRope epilogue.  B is the stacked [Wq; Wk; Wv] with head dim 128;
 // q [M, ldq] receives the rotated queries, kc / vc [*, ldkv] the rotated keys and the values
 // of every slot with slot_kv >= 0 at row slot_kv.  Rotation angles come from table
-// (float2 [positions][64]) at slot_pos; slots with slot_seg < 0 use position 0.
+// (float2 [positions][64]) at slot_pos (0 for slots outside every span).
 struct QkvOut {
     void* q;
     int64_t ldq;
@@ -54,15 +54,16 @@ struct QkvOut {
 
 // bf16 MFMA GEMM.  kStore: C bf16 [M, ldc]; kResidual: C float32 [M, ldc] += A B^T;
 // kSwiGLU: B rows interleaved in blocks of 16 (gate, up) and C bf16 [M, ldc] holds
-// SiLU(gate) * up.  M-tiles whose slots all lie outside every span are skipped when
-// slot_seg is non-null.  Requires N % 256 == 0 and K % 64 == 0.
+// SiLU(gate) * up.  With mtile_m0 only the n_mtiles 256-row tiles starting at those rows are
+// computed (a plan's row-tile list); without it every row.  Requires N % 256 == 0 and
+// K % 64 == 0.
 void gemm_bf16(int epi, const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
-               int M, int N, int K, const int32_t* slot_seg, int capacity, hipStream_t s);
+               int M, int N, int K, const int32_t* mtile_m0, int n_mtiles, hipStream_t s);
 
 // The QKV projection with RoPE and the cache UNPACK in its epilogue (kQkvRope);
-// N = (H + 2 Hkv) * 128, slot_seg required.
+// N = (H + 2 Hkv) * 128; row tiles as gemm_bf16.
 void qkv_rope_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, int M, int K,
-                   const int32_t* slot_seg, int capacity, const QkvOut& out, hipStream_t s);
+                   const int32_t* mtile_m0, int n_mtiles, const QkvOut& out, hipStream_t s);
 
 // float32 FMA GEMM (kStore / kResidual).  Requires K % 16 == 0.
 void gemm_f32(int epi, const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,

@@ -35,17 +35,36 @@ pp_status check_lengths(const int32_t* lengths, int32_t k, int32_t* max_len, int
 pp_status check_plan_buffers(const pp_plan* p, int32_t k, int32_t C) {
     if (!p) return pp::fail(PP_ERR_INVALID_ARG, "plan is NULL");
     if (!p->row_seg_ptr || !p->seg_prompt || !p->seg_start || !p->seg_len || !p->prompt_kv_off ||
-        !p->slot_seg || !p->slot_pos || !p->slot_kv || !p->qtile_seg || !p->qtile_q0)
+        !p->slot_seg || !p->slot_pos || !p->slot_kv || !p->qtile_seg || !p->qtile_q0 || !p->mtile_m0)
         return pp::fail(PP_ERR_INVALID_ARG, "a plan array pointer is NULL");
-    int64_t need_slots = 0, need_q = 0;
-    pp_plan_bounds(k, C, &need_slots, &need_q);
+    int64_t need_slots = 0, need_q = 0, need_m = 0;
+    pp_plan_bounds(k, C, &need_slots, &need_q, &need_m);
     if (p->slot_cap < need_slots)
         return pp::fail(PP_ERR_BUFFER_TOO_SMALL, "slot_cap %lld < %lld (k * C)", (long long)p->slot_cap,
                         (long long)need_slots);
     if (p->qtile_cap < need_q)
         return pp::fail(PP_ERR_BUFFER_TOO_SMALL, "qtile_cap %lld < %lld (k * ceil(C / %d))",
                         (long long)p->qtile_cap, (long long)need_q, PP_QTILE);
+    if (p->mtile_cap < need_m)
+        return pp::fail(PP_ERR_BUFFER_TOO_SMALL, "mtile_cap %lld < %lld (ceil(k * C / %d))",
+                        (long long)p->mtile_cap, (long long)need_m, PP_MTILE);
     return PP_OK;
+}
+
+// Row tiles of the projection GEMMs: the first slot of every PP_MTILE-slot tile of the batch
+// that holds a slot of some span, ascending.  Tiles of row-tail padding alone are left out, so
+// the GEMMs schedule (and balance across the chip) only tiles that have work.
+void build_mtiles(pp_plan* p, int64_t T) {
+    int32_t n = 0;
+    for (int64_t t0 = 0; t0 < T; t0 += PP_MTILE) {
+        const int64_t t1 = std::min<int64_t>(t0 + PP_MTILE, T);
+        for (int64_t t = t0; t < t1; ++t)
+            if (p->slot_seg[t] >= 0) {
+                p->mtile_m0[n++] = static_cast<int32_t>(t0);
+                break;
+            }
+    }
+    p->n_mtiles = n;
 }
 
 // Attention work list: one entry per (segment, query tile), ordered by the number of keys
@@ -76,11 +95,13 @@ void prefix_offsets(const int32_t* lengths, int32_t k, int32_t* off) {
 
 }  // namespace
 
-extern "C" pp_status pp_plan_bounds(int32_t k, int32_t C, int64_t* slot_cap, int64_t* qtile_cap) {
+extern "C" pp_status pp_plan_bounds(int32_t k, int32_t C, int64_t* slot_cap, int64_t* qtile_cap,
+                                    int64_t* mtile_cap) {
     if (k < 0 || C < 0) return pp::fail(PP_ERR_INVALID_ARG, "negative k (%d) or C (%d)", k, C);
-    if (!slot_cap || !qtile_cap) return pp::fail(PP_ERR_INVALID_ARG, "NULL output pointer");
+    if (!slot_cap || !qtile_cap || !mtile_cap) return pp::fail(PP_ERR_INVALID_ARG, "NULL output pointer");
     *slot_cap = int64_t(k) * C;
     *qtile_cap = int64_t(k) * ceil_div(C, PP_QTILE);
+    *mtile_cap = ceil_div(int64_t(k) * C, PP_MTILE);
     return PP_OK;
 }
 
@@ -145,6 +166,7 @@ extern "C" pp_status pp_pack(const int32_t* lengths, int32_t k, int32_t capacity
     plan->max_len = m;
     plan->total_len = static_cast<int32_t>(total);
     build_qtiles(plan, k);
+    build_mtiles(plan, T);
     return PP_OK;
 }
 
@@ -177,5 +199,6 @@ extern "C" pp_status pp_pack_padded(const int32_t* lengths, int32_t k, pp_plan* 
     plan->max_len = m;
     plan->total_len = static_cast<int32_t>(total);
     build_qtiles(plan, k);
+    build_mtiles(plan, T);
     return PP_OK;
 }

@@ -40,16 +40,19 @@ pp_status validate_attention_span(const pp_config* c, const pp_dplan* p) {
 
 pp_status validate_plan(const pp_dplan* p) {
     if (!p) return pp::fail(PP_ERR_INVALID_ARG, "plan is NULL");
-    if (p->k < 0 || p->capacity < 0 || p->n_rows < 0 || p->max_len < 0 || p->total_len < 0 || p->n_qtiles < 0)
+    if (p->k < 0 || p->capacity < 0 || p->n_rows < 0 || p->max_len < 0 || p->total_len < 0 || p->n_qtiles < 0 ||
+        p->n_mtiles < 0)
         return pp::fail(PP_ERR_INVALID_ARG, "plan scalars must be non-negative");
     if (int64_t(p->n_rows) * p->capacity > INT32_MAX)
         return pp::fail(PP_ERR_INVALID_ARG, "n_rows * capacity overflows int32");
-    if (p->total_len > int64_t(p->n_rows) * p->capacity || p->max_len > p->capacity ||
-        (p->total_len > 0 && (p->n_qtiles == 0 || p->max_len == 0)))
+    const int64_t T = int64_t(p->n_rows) * p->capacity;
+    if (p->total_len > T || p->max_len > p->capacity || int64_t(p->n_mtiles) * PP_MTILE >= T + PP_MTILE ||
+        (p->total_len > 0 && (p->n_qtiles == 0 || p->n_mtiles == 0 || p->max_len == 0)))
         return pp::fail(PP_ERR_INVALID_ARG, "inconsistent plan (total_len %d, rows %d x %d, max_len %d)",
                         p->total_len, p->n_rows, p->capacity, p->max_len);
     if (p->total_len > 0 && (!p->seg_prompt || !p->seg_start || !p->seg_len || !p->prompt_kv_off ||
-                             !p->slot_seg || !p->slot_pos || !p->slot_kv || !p->qtile_seg || !p->qtile_q0))
+                             !p->slot_seg || !p->slot_pos || !p->slot_kv || !p->qtile_seg || !p->qtile_q0 ||
+                             !p->mtile_m0))
         return pp::fail(PP_ERR_INVALID_ARG, "a device plan array is NULL");
     return PP_OK;
 }
@@ -161,7 +164,6 @@ extern "C" pp_status pp_prefill(const pp_config* cfg, const pp_weights* w, const
     const int dt = cfg->dtype;
     const bool bf = dt == PP_BF16;
     const int T = plan->n_rows * plan->capacity;
-    const int C = plan->capacity;
     const int d = cfg->d_model, H = cfg->n_heads, Hkv = cfg->n_kv_heads, D = cfg->head_dim, F = cfg->ffn_dim;
     const int qkv_w = (H + 2 * Hkv) * D, hd = H * D, kvw = Hkv * D;
     const float eps = cfg->rms_eps;
@@ -185,10 +187,10 @@ extern "C" pp_status pp_prefill(const pp_config* cfg, const pp_weights* w, const
         ppk::rmsnorm(dt, x, w->attn_norm[l], xn, T, d, eps, s);
         if (bf) {
             const ppk::QkvOut qo{qkv, hd, kc, vc, kvw, table, plan->slot_pos, plan->slot_kv, H, Hkv};
-            ppk::qkv_rope_bf16(xn, d, w->wqkv[l], d, T, d, plan->slot_seg, C, qo, s);
+            ppk::qkv_rope_bf16(xn, d, w->wqkv[l], d, T, d, plan->mtile_m0, plan->n_mtiles, qo, s);
             ppk::attention_bf16(qkv, hd, kc, vc, kvw, attn, hd, plan->seg_prompt, plan->seg_start, plan->seg_len,
                                 plan->prompt_kv_off, plan->qtile_seg, plan->qtile_q0, plan->n_qtiles, H, Hkv, s);
-            ppk::gemm_bf16(ppk::kResidual, attn, hd, w->wo[l], hd, x, d, T, d, hd, plan->slot_seg, C, s);
+            ppk::gemm_bf16(ppk::kResidual, attn, hd, w->wo[l], hd, x, d, T, d, hd, plan->mtile_m0, plan->n_mtiles, s);
         } else {
             float* qkv32 = static_cast<float*>(qkv);
             ppk::gemm_f32(ppk::kStore, static_cast<const float*>(xn), d, static_cast<const float*>(w->wqkv[l]), d,
@@ -203,8 +205,9 @@ extern "C" pp_status pp_prefill(const pp_config* cfg, const pp_weights* w, const
         }
         ppk::rmsnorm(dt, x, w->mlp_norm[l], xn, T, d, eps, s);
         if (bf) {
-            ppk::gemm_bf16(ppk::kSwiGLU, xn, d, w->w_gateup[l], d, act, F, T, 2 * F, d, plan->slot_seg, C, s);
-            ppk::gemm_bf16(ppk::kResidual, act, F, w->w_down[l], F, x, d, T, d, F, plan->slot_seg, C, s);
+            ppk::gemm_bf16(ppk::kSwiGLU, xn, d, w->w_gateup[l], d, act, F, T, 2 * F, d, plan->mtile_m0, plan->n_mtiles,
+                           s);
+            ppk::gemm_bf16(ppk::kResidual, act, F, w->w_down[l], F, x, d, T, d, F, plan->mtile_m0, plan->n_mtiles, s);
         } else {
             ppk::gemm_f32(ppk::kStore, static_cast<const float*>(xn), d, static_cast<const float*>(w->w_gateup[l]), d,
                           gu, 2 * F, T, 2 * F, d, s);
@@ -288,15 +291,15 @@ extern "C" pp_status pp_gemm(int32_t dtype, int32_t epilogue, const void* A, int
         if (dtype != PP_BF16) return pp::fail(PP_ERR_UNSUPPORTED, "row-tile skipping is a bf16 GEMM feature");
         if (int64_t(M) != int64_t(plan->n_rows) * plan->capacity)
             return pp::fail(PP_ERR_INVALID_ARG, "M %d != n_rows * capacity of the plan", M);
-        if (M > 0 && !plan->slot_seg) return pp::fail(PP_ERR_INVALID_ARG, "plan slot_seg is NULL");
+        if (M > 0 && !plan->mtile_m0) return pp::fail(PP_ERR_INVALID_ARG, "plan mtile_m0 is NULL");
     }
     if (M == 0) return PP_OK;
     if (!A || !B || !C) return pp::fail(PP_ERR_INVALID_ARG, "NULL buffer");
     (void)hipGetLastError();
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (dtype == PP_BF16)
-        ppk::gemm_bf16(epilogue, A, lda, B, ldb, C, ldc, M, N, K, plan ? plan->slot_seg : nullptr,
-                       plan ? plan->capacity : 0, s);
+        ppk::gemm_bf16(epilogue, A, lda, B, ldb, C, ldc, M, N, K, plan ? plan->mtile_m0 : nullptr,
+                       plan ? plan->n_mtiles : 0, s);
     else
         ppk::gemm_f32(epilogue, static_cast<const float*>(A), lda, static_cast<const float*>(B), ldb,
                       static_cast<float*>(C), ldc, M, N, K, s);
@@ -323,7 +326,7 @@ extern "C" pp_status pp_qkv_projection(const pp_config* cfg, const pp_dplan* pla
     ppk::rope_table(tab, plan->max_len, D, cfg->rope_theta, s);
     const ppk::QkvOut qo{q_out, int64_t(H) * D, k_cache, v_cache, int64_t(Hkv) * D, tab, plan->slot_pos,
                          plan->slot_kv, H, Hkv};
-    ppk::qkv_rope_bf16(xn, d, wqkv, d, T, d, plan->slot_seg, plan->capacity, qo, s);
+    ppk::qkv_rope_bf16(xn, d, wqkv, d, T, d, plan->mtile_m0, plan->n_mtiles, qo, s);
     return finish("qkv_projection");
 }
 

@@ -23,6 +23,7 @@ PP_OK, PP_ERR_INVALID_ARG, PP_ERR_TOO_LONG, PP_ERR_BUFFER_TOO_SMALL, PP_ERR_UNSU
 PP_F32, PP_BF16 = 0, 1
 PP_EPI_STORE, PP_EPI_RESIDUAL, PP_EPI_SWIGLU = 0, 1, 2
 PP_QTILE = 128
+PP_MTILE = 256
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
 
@@ -40,10 +41,11 @@ class PrepackError(RuntimeError):
 class PPPlan(ctypes.Structure):
     _fields_ = [("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("n_rows", ctypes.c_int32),
                 ("max_len", ctypes.c_int32), ("total_len", ctypes.c_int32), ("n_qtiles", ctypes.c_int32),
-                ("slot_cap", ctypes.c_int64), ("qtile_cap", ctypes.c_int64),
+                ("n_mtiles", ctypes.c_int32), ("slot_cap", ctypes.c_int64), ("qtile_cap", ctypes.c_int64),
+                ("mtile_cap", ctypes.c_int64),
                 ("row_seg_ptr", _i32p), ("seg_prompt", _i32p), ("seg_start", _i32p), ("seg_len", _i32p),
                 ("prompt_kv_off", _i32p), ("slot_seg", _i32p), ("slot_pos", _i32p), ("slot_kv", _i32p),
-                ("qtile_seg", _i32p), ("qtile_q0", _i32p)]
+                ("qtile_seg", _i32p), ("qtile_q0", _i32p), ("mtile_m0", _i32p)]
 
 
 class PPConfig(ctypes.Structure):
@@ -63,9 +65,11 @@ class PPWeights(ctypes.Structure):
 class PPDPlan(ctypes.Structure):
     _fields_ = [("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("n_rows", ctypes.c_int32),
                 ("max_len", ctypes.c_int32), ("total_len", ctypes.c_int32), ("n_qtiles", ctypes.c_int32),
+                ("n_mtiles", ctypes.c_int32),
                 ("seg_prompt", ctypes.c_void_p), ("seg_start", ctypes.c_void_p), ("seg_len", ctypes.c_void_p),
                 ("prompt_kv_off", ctypes.c_void_p), ("slot_seg", ctypes.c_void_p), ("slot_pos", ctypes.c_void_p),
-                ("slot_kv", ctypes.c_void_p), ("qtile_seg", ctypes.c_void_p), ("qtile_q0", ctypes.c_void_p)]
+                ("slot_kv", ctypes.c_void_p), ("qtile_seg", ctypes.c_void_p), ("qtile_q0", ctypes.c_void_p),
+                ("mtile_m0", ctypes.c_void_p)]
 
 
 class PPGenLayout(ctypes.Structure):
@@ -94,6 +98,7 @@ def lib() -> ctypes.CDLL:
         L.pp_last_error.restype = ctypes.c_char_p
         L.pp_version.restype = ctypes.c_char_p
         L.pp_plan_bounds.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+                                     ctypes.POINTER(ctypes.c_int64),
                                      ctypes.POINTER(ctypes.c_int64)]
         L.pp_pack.argtypes = [_i32p, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(PPPlan)]
         L.pp_pack_padded.argtypes = [_i32p, ctypes.c_int32, ctypes.POINTER(PPPlan)]
@@ -161,6 +166,7 @@ class Plan:
     slot_kv: np.ndarray
     qtile_seg: np.ndarray
     qtile_q0: np.ndarray
+    mtile_m0: np.ndarray
 
     @property
     def n_slots(self) -> int:
@@ -170,30 +176,44 @@ class Plan:
     def n_qtiles(self) -> int:
         return int(self.qtile_seg.size)
 
+    @property
+    def n_mtiles(self) -> int:
+        return int(self.mtile_m0.size)
+
 
 def pp_plan_bounds(k: int, C: int):
-    s, q = ctypes.c_int64(), ctypes.c_int64()
-    _check(lib().pp_plan_bounds(k, C, ctypes.byref(s), ctypes.byref(q)), "pp_plan_bounds")
-    return s.value, q.value
+    """(slot_cap, qtile_cap, mtile_cap) of a plan of k prompts in rows of C slots."""
+    s, q, m = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().pp_plan_bounds(k, C, ctypes.byref(s), ctypes.byref(q), ctypes.byref(m)), "pp_plan_bounds")
+    return s.value, q.value, m.value
+
+
+_PLAN_ARRAYS = ("row_seg_ptr", "seg_prompt", "seg_start", "seg_len", "prompt_kv_off", "slot_seg", "slot_pos",
+                "slot_kv", "qtile_seg", "qtile_q0", "mtile_m0")
+
+
+def _plan_arrays(k: int, bs: int, bq: int, bm: int):
+    sizes = {"row_seg_ptr": k + 1, "seg_prompt": k, "seg_start": k, "seg_len": k, "prompt_kv_off": k + 1,
+             "slot_seg": bs, "slot_pos": bs, "slot_kv": bs, "qtile_seg": bq, "qtile_q0": bq, "mtile_m0": bm}
+    return {n: np.empty(max(sizes[n], 1), dtype=np.int32) for n in _PLAN_ARRAYS}
 
 
 def _ptr(a: np.ndarray):
     return a.ctypes.data_as(_i32p)
 
 
-def _run_pack(lengths: Sequence[int], capacity: Optional[int], slot_cap=None, qtile_cap=None) -> Plan:
+def _run_pack(lengths: Sequence[int], capacity: Optional[int], slot_cap=None, qtile_cap=None,
+              mtile_cap=None) -> Plan:
     L = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
     k = int(L.size)
     m = int(L.max()) if k else 0
     C = m if (capacity is None or capacity == 0) else int(capacity)
-    bs, bq = pp_plan_bounds(k, max(C, 0)) if C >= 0 else (0, 0)
+    bs, bq, bm = pp_plan_bounds(k, max(C, 0)) if C >= 0 else (0, 0, 0)
     bs = bs if slot_cap is None else slot_cap
     bq = bq if qtile_cap is None else qtile_cap
-    arrs = {n: np.empty(max(size, 1), dtype=np.int32) for n, size in
-            [("row_seg_ptr", k + 1), ("seg_prompt", k), ("seg_start", k), ("seg_len", k),
-             ("prompt_kv_off", k + 1), ("slot_seg", bs), ("slot_pos", bs), ("slot_kv", bs),
-             ("qtile_seg", bq), ("qtile_q0", bq)]}
-    p = PPPlan(slot_cap=bs, qtile_cap=bq, **{n: _ptr(a) for n, a in arrs.items()})
+    bm = bm if mtile_cap is None else mtile_cap
+    arrs = _plan_arrays(k, bs, bq, bm)
+    p = PPPlan(slot_cap=bs, qtile_cap=bq, mtile_cap=bm, **{n: _ptr(a) for n, a in arrs.items()})
     if capacity is None:
         _check(lib().pp_pack_padded(_ptr(L) if k else None, k, ctypes.byref(p)), "pp_pack_padded")
     else:
@@ -204,7 +224,8 @@ def _run_pack(lengths: Sequence[int], capacity: Optional[int], slot_cap=None, qt
                 seg_start=arrs["seg_start"][:k].copy(), seg_len=arrs["seg_len"][:k].copy(),
                 prompt_kv_off=arrs["prompt_kv_off"][: k + 1].copy(), slot_seg=arrs["slot_seg"][:T].copy(),
                 slot_pos=arrs["slot_pos"][:T].copy(), slot_kv=arrs["slot_kv"][:T].copy(),
-                qtile_seg=arrs["qtile_seg"][: p.n_qtiles].copy(), qtile_q0=arrs["qtile_q0"][: p.n_qtiles].copy())
+                qtile_seg=arrs["qtile_seg"][: p.n_qtiles].copy(), qtile_q0=arrs["qtile_q0"][: p.n_qtiles].copy(),
+                mtile_m0=arrs["mtile_m0"][: p.n_mtiles].copy())
 
 
 class PlanBuffers:
@@ -213,13 +234,10 @@ class PlanBuffers:
     struct; its arrays stay valid until the next call)."""
 
     def __init__(self, k: int, C: int):
-        bs, bq = pp_plan_bounds(k, C)
+        bs, bq, bm = pp_plan_bounds(k, C)
         self.k = k
-        self.arrs = {n: np.empty(max(size, 1), dtype=np.int32) for n, size in
-                     [("row_seg_ptr", k + 1), ("seg_prompt", k), ("seg_start", k), ("seg_len", k),
-                      ("prompt_kv_off", k + 1), ("slot_seg", bs), ("slot_pos", bs), ("slot_kv", bs),
-                      ("qtile_seg", bq), ("qtile_q0", bq)]}
-        self.struct = PPPlan(slot_cap=bs, qtile_cap=bq, **{n: _ptr(a) for n, a in self.arrs.items()})
+        self.arrs = _plan_arrays(k, bs, bq, bm)
+        self.struct = PPPlan(slot_cap=bs, qtile_cap=bq, mtile_cap=bm, **{n: _ptr(a) for n, a in self.arrs.items()})
 
     def pack(self, lengths: np.ndarray, capacity: int) -> PPPlan:
         """pp_pack of int32 contiguous ``lengths`` (at most k of them, rows of at most C)."""
@@ -252,9 +270,9 @@ class DevicePlan:
         self.plan = plan
         self.tensors = {n: torch.from_numpy(np.ascontiguousarray(getattr(plan, n))).to(device)
                         for n in ("seg_prompt", "seg_start", "seg_len", "prompt_kv_off", "slot_seg", "slot_pos",
-                                  "slot_kv", "qtile_seg", "qtile_q0")}
+                                  "slot_kv", "qtile_seg", "qtile_q0", "mtile_m0")}
         self.struct = PPDPlan(k=plan.k, capacity=plan.capacity, n_rows=plan.n_rows, max_len=plan.max_len,
-                              total_len=plan.total_len, n_qtiles=plan.n_qtiles,
+                              total_len=plan.total_len, n_qtiles=plan.n_qtiles, n_mtiles=plan.n_mtiles,
                               **{n: t.data_ptr() for n, t in self.tensors.items()})
 
 

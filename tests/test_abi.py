@@ -42,9 +42,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_struct_layouts_match_header():
-    assert ctypes.sizeof(pp.PPPlan) == 6 * 4 + 2 * 8 + 10 * 8
+    assert ctypes.sizeof(pp.PPPlan) == 8 * 4 + 3 * 8 + 11 * 8     # 7 int32 + padding to 8 bytes
     assert ctypes.sizeof(pp.PPConfig) == 10 * 4
-    assert ctypes.sizeof(pp.PPDPlan) == 6 * 4 + 9 * 8
+    assert ctypes.sizeof(pp.PPDPlan) == 8 * 4 + 10 * 8
     assert ctypes.sizeof(pp.PPWeights) == 8 * 8
 
 
@@ -60,6 +60,9 @@ def _check_work_list(plan):
     assert got == want
     keys = [min(q0 + pp.PP_QTILE, int(plan.seg_len[s])) for s, q0 in zip(plan.qtile_seg, plan.qtile_q0)]
     assert all(a >= b for a, b in zip(keys, keys[1:]))
+    # GEMM row tiles: exactly the PP_MTILE-slot tiles holding a slot of some span, ascending
+    want_m = [t0 for t0 in range(0, plan.n_slots, pp.PP_MTILE) if (plan.slot_seg[t0:t0 + pp.PP_MTILE] >= 0).any()]
+    assert plan.mtile_m0.tolist() == want_m
 
 
 def _same(plan, ref):
@@ -137,7 +140,10 @@ def test_errors(L):
     # NULL plan
     lengths = (ctypes.c_int32 * 2)(3, 4)
     assert pp.lib().pp_pack(lengths, 2, 8, None) == pp.PP_ERR_INVALID_ARG
-    assert pp.lib().pp_plan_bounds(-1, 4, None, None) == pp.PP_ERR_INVALID_ARG
+    assert pp.lib().pp_plan_bounds(-1, 4, None, None, None) == pp.PP_ERR_INVALID_ARG
+    with pytest.raises(pp.PrepackError) as e:
+        pp.pp_pack([300, 200, 300], 512, mtile_cap=2)            # needs ceil(3 * 512 / 256) = 6
+    assert e.value.code == pp.PP_ERR_BUFFER_TOO_SMALL
 
 
 def _cfg(**kw):
@@ -148,9 +154,9 @@ def _cfg(**kw):
 
 
 def _dplan(**kw):
-    base = dict(k=2, capacity=256, n_rows=2, max_len=200, total_len=300, n_qtiles=3,
+    base = dict(k=2, capacity=256, n_rows=2, max_len=200, total_len=300, n_qtiles=3, n_mtiles=2,
                 **{n: 0x1000 for n in ("seg_prompt", "seg_start", "seg_len", "prompt_kv_off", "slot_seg",
-                                       "slot_pos", "slot_kv", "qtile_seg", "qtile_q0")})
+                                       "slot_pos", "slot_kv", "qtile_seg", "qtile_q0", "mtile_m0")})
     base.update(kw)
     return pp.PPDPlan(**base)
 
@@ -183,6 +189,9 @@ def test_workspace_size_and_config_validation(L):
     assert _ws(_cfg(), _dplan(slot_kv=0))[0] == pp.PP_ERR_INVALID_ARG            # NULL device array
     assert _ws(_cfg(), _dplan(prompt_kv_off=0))[0] == pp.PP_ERR_INVALID_ARG
     assert _ws(_cfg(), _dplan(seg_prompt=0))[0] == pp.PP_ERR_INVALID_ARG
+    assert _ws(_cfg(), _dplan(mtile_m0=0))[0] == pp.PP_ERR_INVALID_ARG
+    assert _ws(_cfg(), _dplan(n_mtiles=0))[0] == pp.PP_ERR_INVALID_ARG            # tokens but no row tile
+    assert _ws(_cfg(), _dplan(n_mtiles=3))[0] == pp.PP_ERR_INVALID_ARG            # more tiles than 512 slots hold
 
 
 def _weights(n_layers):
@@ -213,7 +222,7 @@ def test_prefill_rejects_before_enqueue(L):
     assert f(*args(0x10000, need)) == pp.PP_ERR_INVALID_ARG
     assert "layer 0" in pp.pp_last_error()
     # an empty plan is a no-op that succeeds without touching any pointer
-    empty = _dplan(k=0, n_rows=0, capacity=0, max_len=0, total_len=0, n_qtiles=0)
+    empty = _dplan(k=0, n_rows=0, capacity=0, max_len=0, total_len=0, n_qtiles=0, n_mtiles=0)
     w2, keep2 = _weights(1)
     assert f(ctypes.byref(cfg), ctypes.byref(w2), ctypes.byref(empty), None, None, 0, None, None, None,
              None) == pp.PP_OK

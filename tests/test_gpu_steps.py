@@ -71,6 +71,38 @@ def test_gemm_bf16_swiglu(M, F, K):
     check_bar(f"gemm swiglu {M}x{F}x{K}", got, ref)
 
 
+@pytest.mark.parametrize("epi", [pp.PP_EPI_STORE, pp.PP_EPI_RESIDUAL])
+def test_gemm_bf16_plan_row_tiles(epi):
+    """With a plan, the GEMM computes exactly the plan's row tiles: every slot of a prompt is
+    correct, and rows of tiles made of row-tail padding alone keep what they held."""
+    plan = pp.pp_pack([700, 700, 700, 600, 600, 600, 300], 1024)   # pad-only tiles mid-batch
+    T, N, K = plan.n_slots, 4096, 2048
+    assert plan.n_mtiles < T // 256                            # some tiles are padding only
+    rng = np.random.default_rng([T, epi])
+    A, B = rand_bf16(rng, (T, K)), rand_bf16(rng, (N, K), 0.02)
+    if epi == pp.PP_EPI_STORE:
+        C = torch.full((T, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+        base = None
+    else:
+        base = rng.standard_normal((T, N)).astype(np.float32)
+        C = f32_dev(base)
+    pp.pp_gemm(pp.PP_BF16, epi, bf16_dev(A), K, bf16_dev(B), K, C, N, T, N, K, pp.DevicePlan(plan))
+    got = host64(C)
+    covered = np.zeros(T, dtype=bool)
+    for m0 in plan.mtile_m0:
+        covered[m0:m0 + 256] = True
+    assert covered[plan.slot_seg >= 0].all()
+    rows = np.nonzero(covered)[0]
+    ref = A[rows].astype(np.float64) @ B.astype(np.float64).T
+    if epi == pp.PP_EPI_STORE:
+        assert within_ulps(got[rows], ref, 1.0, 1e-6) <= 1.0
+        assert np.isnan(got[~covered]).all()
+    else:
+        ref += base[rows]
+        assert D.errors(got[rows], ref)[0] <= 2e-4
+        assert np.array_equal(got[~covered], base[~covered].astype(np.float64))
+
+
 def test_gemm_f32():
     rng = np.random.default_rng(7)
     M, N, K = 77, 1376, 688
