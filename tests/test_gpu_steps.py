@@ -120,6 +120,7 @@ ATTN_CASES = [
     ([1, 5, 64, 127, 128, 129, 300, 700], 1024, 32, 32),
     ([40, 200, 513, 1, 1000], 1024, 32, 8),
     ([2048], 2048, 16, 16),
+    ([31, 32, 33, 95, 96, 97, 160, 191, 192, 193], 1024, 16, 4),   # around each wavefront's 32 queries
 ]
 
 
