@@ -29,7 +29,10 @@ __global__ void rope_table_kernel(float2* __restrict__ table, int64_t n, int hal
 }
 
 // ------------------------------------------------------------------------------- embedding
-template <typename TE>
+// NC > 0: d == NC * 512 (8 elements per lane per chunk); every load of the row is issued
+// before the first store, so a wavefront has the whole row in flight.  NC == 0: any d that
+// is a multiple of 8, one chunk at a time.
+template <typename TE, int NC>
 __global__ __launch_bounds__(kBlock) void embed_kernel(float* __restrict__ x, const TE* __restrict__ E,
                                                        const int32_t* __restrict__ tokens,
                                                        const int32_t* __restrict__ slot_kv, int T, int d,
@@ -40,18 +43,43 @@ __global__ __launch_bounds__(kBlock) void embed_kernel(float* __restrict__ x, co
     float* xr = x + row * d;
     const int kv = slot_kv[row];
     const int tok = kv < 0 ? -1 : tokens[kv];
-    float v[8];
     if (tok < 0 || tok >= vocab) {  // pad slot, or a token id outside the vocabulary
+        float z[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = 0.f;
-        for (int c = lane * 8; c < d; c += kWave * 8) store8(xr + c, v);
+        for (int i = 0; i < 8; ++i) z[i] = 0.f;
+        for (int c = lane * 8; c < d; c += kWave * 8) store8(xr + c, z);
         return;
     }
     const TE* er = E + int64_t(tok) * d;
-    for (int c = lane * 8; c < d; c += kWave * 8) {
-        load8(er + c, v);
-        store8(xr + c, v);
+    if constexpr (NC > 0) {
+        float v[NC][8];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) load8(er + c * 512 + lane * 8, v[c]);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) store8(xr + c * 512 + lane * 8, v[c]);
+    } else {
+        float v[8];
+        for (int c = lane * 8; c < d; c += kWave * 8) {
+            load8(er + c, v);
+            store8(xr + c, v);
+        }
     }
+}
+
+template <typename TE>
+void embed_dispatch(float* x, const TE* E, int vocab, const int32_t* tokens, const int32_t* slot_kv, int T, int d,
+                    hipStream_t s) {
+    const dim3 grid((T + kRowsPerBlock - 1) / kRowsPerBlock);
+    const int nc = d % 512 == 0 ? d / 512 : 0;
+#define PP_EMB(NC) embed_kernel<TE, NC><<<grid, kBlock, 0, s>>>(x, E, tokens, slot_kv, T, d, vocab)
+    switch (nc) {
+        case 2: PP_EMB(2); break;
+        case 4: PP_EMB(4); break;
+        case 8: PP_EMB(8); break;
+        case 16: PP_EMB(16); break;
+        default: PP_EMB(0); break;
+    }
+#undef PP_EMB
 }
 
 // ------------------------------------------------------------------------------- RMSNorm
@@ -204,11 +232,10 @@ void rope_table(float2* table, int P, int D, float theta, hipStream_t s) {
 
 void embed(int dtype, float* x, const void* E, int vocab, const int32_t* tokens, const int32_t* slot_kv, int T,
            int d, hipStream_t s) {
-    const dim3 grid((T + kRowsPerBlock - 1) / kRowsPerBlock);
     if (dtype == PP_BF16)
-        embed_kernel<bf16><<<grid, kBlock, 0, s>>>(x, static_cast<const bf16*>(E), tokens, slot_kv, T, d, vocab);
+        embed_dispatch(x, static_cast<const bf16*>(E), vocab, tokens, slot_kv, T, d, s);
     else
-        embed_kernel<float><<<grid, kBlock, 0, s>>>(x, static_cast<const float*>(E), tokens, slot_kv, T, d, vocab);
+        embed_dispatch(x, static_cast<const float*>(E), vocab, tokens, slot_kv, T, d, s);
 }
 
 void rmsnorm(int dtype, const float* x, const float* g, void* out, int T, int d, float eps, hipStream_t s) {

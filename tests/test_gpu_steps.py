@@ -333,9 +333,10 @@ def test_rmsnorm(d, dtype):
 
 
 @pytest.mark.parametrize("dtype", [pp.PP_BF16, pp.PP_F32])
-def test_embed_gather_bit_exact(dtype):
+@pytest.mark.parametrize("d", [256, 1024, 2048, 4096])         # generic loop; 2, 4, 8 chunks of 512
+def test_embed_gather_bit_exact(dtype, d):
     rng = np.random.default_rng(5)
-    V, d = 1000, 256
+    V = 1000
     lengths = [5, 17, 1, 40]
     plan = pp.pp_pack(lengths, 64)
     E = rand_bf16(rng, (V, d), 0.02) if dtype == pp.PP_BF16 else rng.standard_normal((V, d)).astype(np.float32)
