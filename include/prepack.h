@@ -72,7 +72,9 @@ const char* pp_version(void);
  *   qtile_seg     [qtile_cap] attention work list: segment of each query tile
  *   qtile_q0      [qtile_cap] first query (offset inside the segment) of each query tile;
  *                             every (segment, multiple of PP_QTILE below seg_len) appears
- *                             once, tiles with more keys to visit first
+ *                             once; the tiles of a segment are consecutive, segments longest
+ *                             first (ties: lower segment index), inside a segment the tile
+ *                             with the highest first query first
  *   mtile_m0      [mtile_cap] row tiles of the projection GEMMs: the first slot of every
  *                             PP_MTILE-slot tile of the batch (slots t0 .. t0 + PP_MTILE - 1,
  *                             t0 a multiple of PP_MTILE) holding a slot of some span,

@@ -29,8 +29,10 @@
 //     (ds_read_b64_tr_b16), with key rows chosen so that its key order matches the order in
 //     which the S^T accumulators hold the probabilities: P feeds the MFMA from registers
 //     as is;
-//   * query heads sharing a KV head (GQA) are adjacent workgroups, so their K/V tiles come
-//     from L2.
+//   * the work list keeps each prompt's query tiles together, and the workgroups of one
+//     work item (one per query head) are spread so that each XCD serves whole KV heads: the
+//     tiles of a prompt that read the same keys and values run at the same time on the same
+//     XCD and share its L2.
 // float32 kernel: one wavefront per (query slot, head), a plain online-softmax loop over
 // the query's keys, used for float32 models.
 #include "device.h"
@@ -78,7 +80,16 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(const bf16* __restrict
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int w = blockIdx.x / H, h = blockIdx.x - (blockIdx.x / H) * H;
+    const int w = blockIdx.x / H, j = blockIdx.x - (blockIdx.x / H) * H;
+    // Workgroups are dealt to the 8 XCDs round-robin (XCD = workgroup id % 8), and work item w
+    // takes ids w H .. w H + H - 1.  When the KV heads split evenly over the XCDs, the query
+    // heads sharing a KV head are placed on one XCD (id % 8 = j % 8 picks the KV head's XCD),
+    // so that its L2 serves their common keys and values; otherwise head j.
+    int h = j;
+    if (Hkv % 8 == 0) {
+        const int G = H / Hkv, x = j & 7, a = j >> 3;
+        h = (x + 8 * (a / G)) * G + a % G;
+    }
     const int seg = qtile_seg[w], q0 = qtile_q0[w];
     const int a = seg_start[seg], n = seg_len[seg];
     const int prompt = seg_prompt[seg];

@@ -67,19 +67,23 @@ void build_mtiles(pp_plan* p, int64_t T) {
     p->n_mtiles = n;
 }
 
-// Attention work list: one entry per (segment, query tile), ordered by the number of keys
-// the tile's last query sees, largest first (longest-processing-time-first), ties by
-// segment then offset.  The set is fixed by the segments; the order only balances load.
+// Attention work list: one entry per (segment, query tile).  The tiles of a segment are
+// consecutive, segments longest first (ties by segment index), and inside a segment the tiles
+// with more keys to visit come first (the last query tile first).  The set is fixed by the
+// segments; the order serves the kernel: the tiles of one prompt, which all read the same
+// keys and values, run at the same time on the same XCD (its L2 serves the re-reads), and
+// long work starts first.
 void build_qtiles(pp_plan* p, int32_t n_seg) {
     struct T { int32_t work, seg, q0; };
     std::vector<T> tiles;
     for (int32_t s = 0; s < n_seg; ++s)
         for (int32_t q0 = 0; q0 < p->seg_len[s]; q0 += PP_QTILE)
             tiles.push_back({std::min(q0 + PP_QTILE, p->seg_len[s]), s, q0});
-    std::stable_sort(tiles.begin(), tiles.end(), [](const T& a, const T& b) {
-        if (a.work != b.work) return a.work > b.work;
+    const int32_t* len = p->seg_len;
+    std::stable_sort(tiles.begin(), tiles.end(), [len](const T& a, const T& b) {
+        if (len[a.seg] != len[b.seg]) return len[a.seg] > len[b.seg];
         if (a.seg != b.seg) return a.seg < b.seg;
-        return a.q0 < b.q0;
+        return a.work > b.work;
     });
     for (size_t i = 0; i < tiles.size(); ++i) {
         p->qtile_seg[i] = tiles[i].seg;

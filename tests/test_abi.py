@@ -54,12 +54,13 @@ def test_version(L):
 
 def _check_work_list(plan):
     """The attention work list as include/prepack.h states it: every (segment, multiple of
-    PP_QTILE below the segment's length) exactly once, tiles with more keys to visit first."""
-    got = sorted(zip(plan.qtile_seg.tolist(), plan.qtile_q0.tolist()))
-    want = sorted((s, q0) for s in range(plan.k) for q0 in range(0, int(plan.seg_len[s]), pp.PP_QTILE))
+    PP_QTILE below the segment's length) exactly once; a segment's tiles consecutive, segments
+    longest first (ties by index), inside a segment the highest first query first."""
+    got = list(zip(plan.qtile_seg.tolist(), plan.qtile_q0.tolist()))
+    assert sorted(got) == sorted((s, q0) for s in range(plan.k) for q0 in range(0, int(plan.seg_len[s]), pp.PP_QTILE))
+    segs = sorted(range(plan.k), key=lambda s: (-int(plan.seg_len[s]), s))
+    want = [(s, q0) for s in segs for q0 in reversed(range(0, int(plan.seg_len[s]), pp.PP_QTILE))]
     assert got == want
-    keys = [min(q0 + pp.PP_QTILE, int(plan.seg_len[s])) for s, q0 in zip(plan.qtile_seg, plan.qtile_q0)]
-    assert all(a >= b for a, b in zip(keys, keys[1:]))
     # GEMM row tiles: exactly the PP_MTILE-slot tiles holding a slot of some span, ascending
     want_m = [t0 for t0 in range(0, plan.n_slots, pp.PP_MTILE) if (plan.slot_seg[t0:t0 + pp.PP_MTILE] >= 0).any()]
     assert plan.mtile_m0.tolist() == want_m
