@@ -341,7 +341,8 @@ def test_embed_gather_bit_exact(dtype, d):
     plan = pp.pp_pack(lengths, 64)
     E = rand_bf16(rng, (V, d), 0.02) if dtype == pp.PP_BF16 else rng.standard_normal((V, d)).astype(np.float32)
     toks = rng.integers(0, V, sum(lengths)).astype(np.int32)
-    toks[3] = V + 5                          # out of range -> zero row
+    toks[3] = V + 5                          # out of range -> zero row (include/prepack.h)
+    toks[9] = -3                             # negative: also a zero row
     Ed = bf16_dev(E) if dtype == pp.PP_BF16 else f32_dev(E)
     x = torch.full((plan.n_slots, d), float("nan"), dtype=torch.float32, device="cuda")
     pp.pp_embed(dtype, Ed, V, d, i32_dev(toks), pp.DevicePlan(plan), x)
@@ -349,7 +350,7 @@ def test_embed_gather_bit_exact(dtype, d):
     want = np.zeros((plan.n_slots, d))
     real = plan.slot_kv >= 0
     ids = toks[plan.slot_kv[real]]
-    ok = ids < V
+    ok = (ids >= 0) & (ids < V)
     rows = np.nonzero(real)[0]
     want[rows[ok]] = E[ids[ok]]
     assert np.array_equal(got, want)
