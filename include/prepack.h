@@ -177,7 +177,9 @@ typedef struct pp_weights {
 
 /* A plan copied to device memory: the scalars of pp_plan and device copies of the arrays
  * the kernels read (same meaning and length as in pp_plan; slot arrays hold
- * n_rows * capacity entries, qtile arrays n_qtiles, mtile_m0 n_mtiles). */
+ * n_rows * capacity entries, qtile arrays n_qtiles, mtile_m0 n_mtiles).  The scalars are
+ * validated on the host; the arrays' contents are trusted to be what pp_pack or
+ * pp_pack_padded wrote (the kernels index memory with them). */
 typedef struct pp_dplan {
     int32_t k, capacity, n_rows, max_len, total_len, n_qtiles, n_mtiles;
     const int32_t* seg_prompt;
