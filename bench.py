@@ -502,6 +502,47 @@ def run_generate(args):
     print(json.dumps(out), flush=True)
 
 
+def run_attention_lengths(args):
+    """pp_attention alone on batches of equal-length prompts filling 32,768 slots (rows of 4096),
+    Llama-2-7B heads (32 x 128), random bf16 queries, keys and values: time per call against
+    both rooflines of the kernel.  Algorithmic work per head: 4 D l(l+1)/2 FLOP per prompt;
+    algorithmic bytes: every token's query, key, value and output once (4 x 2 D bytes per token
+    and head).  Key/value re-reads by later query tiles are not algorithmic."""
+    import numpy as np
+    import torch
+
+    from paper_2404_09529_amd import prepack as pp
+    H, D, slots = 32, 128, 32768
+    cfg = pp.PPConfig(n_layers=1, d_model=H * D, n_heads=H, n_kv_heads=H, head_dim=D, ffn_dim=11008, vocab=32000,
+                      dtype=pp.PP_BF16, rms_eps=1e-5, rope_theta=1e4)
+    out = {"sweep": "attention-lengths", "heads": H, "head_dim": D, "slots": slots, "rows": []}
+    g = torch.Generator(device="cuda").manual_seed(args.seed)
+    for n in [int(x) for x in args.lengths.split(",")]:
+        lengths = np.full(slots // n, n, dtype=np.int32)
+        plan = pp.pp_pack(lengths, 4096)
+        dp = pp.DevicePlan(plan)
+        q = torch.randn((plan.n_slots, H * D), generator=g, device="cuda").to(torch.bfloat16)
+        kc = torch.randn((plan.total_len, H * D), generator=g, device="cuda").to(torch.bfloat16)
+        vc = torch.randn((plan.total_len, H * D), generator=g, device="cuda").to(torch.bfloat16)
+        o = torch.empty_like(q)
+        t = time_steps(lambda: pp.pp_attention(cfg, dp, q, H * D, kc, vc, o), args.reps, args.sweep_warmup)
+        ms = t["ms_median"]
+        pairs = attention_pairs(plan, lengths)
+        flop = 4 * H * D * pairs["algorithmic"]
+        nbytes = 4 * 2 * D * H * plan.total_len
+        rec = {"length": n, "prompts": int(len(lengths)), "us": round(ms * 1e3, 1),
+               "tflops": round(flop / (ms / 1e3) / 1e12, 1), "frac_mfma": round(flop / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+               "gbps": round(nbytes / (ms / 1e3) / 1e9, 1), "frac_hbm": round(nbytes / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS, 4),
+               "bound_us": round(1e6 * max(flop / (PEAK_BF16_TFLOPS * 1e12), nbytes / (PEAK_HBM_GBPS * 1e9)), 1),
+               "pairs_executed_over_algorithmic": pairs["inflation"]}
+        out["rows"].append(rec)
+        log(f"attention, prompts of {n}: {rec['us']} us, {rec['tflops']} TFLOP/s ({100 * rec['frac_mfma']:.1f}% of MFMA "
+            f"peak), {rec['gbps']} GB/s algorithmic ({100 * rec['frac_hbm']:.1f}% of HBM)")
+        del q, kc, vc, o
+        torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+
+
 def run_sweep(args):
     """--sweep regression: batches of --batch prompts from the prompt pool, the speedup of
     packing over full batching per batch, and the linear fits of the speedup on r/k and on
@@ -593,11 +634,12 @@ def main():
                     help="run only the dominant kernel and the calibration copy (for counter passes)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with the calibration copy (for byte-counter passes over the whole step)")
-    ap.add_argument("--sweep", choices=["regression", "batch", "datasets", "dataset-packing"],
+    ap.add_argument("--sweep", choices=["regression", "batch", "datasets", "dataset-packing", "attention-lengths"],
                     help="instead of the benchmark line: packing against full batching per batch of a prompt "
                          "pool, with linear fits of the speedup (regression), across batch sizes (batch), with "
                          "the time to first token over dataset stand-ins (datasets), or against length-ordered "
-                         "batching and whole-set packing (dataset-packing)")
+                         "batching and whole-set packing (dataset-packing); attention-lengths: the attention kernel "
+                         "alone on prompts of each of --lengths against its MFMA and HBM rooflines")
     ap.add_argument("--pool", default="uniform", help="sweep regression/batch: uniform (U[1,512]) or a dataset "
                                                      "stand-in (wiki256, wiki512, mmlu, hh-rlhf, alpaca, samsum)")
     ap.add_argument("--pools", default="wiki256,wiki512,mmlu,hh-rlhf,alpaca,samsum",
@@ -606,6 +648,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0, help="sweep: decoder layers (0 = the model's full depth)")
     ap.add_argument("--batch", type=int, default=32, help="sweep: prompts (dataset packing: rows) per batch")
     ap.add_argument("--batch-sizes", default="1,2,4,8,16,32,64", help="sweep batch: batch sizes")
+    ap.add_argument("--lengths", default="16,32,64,128,256,512,1024,2048,4096",
+                    help="sweep attention-lengths: prompt lengths (each batch fills 32,768 slots)")
     ap.add_argument("--prompts", type=int, default=5000, help="sweep: prompts taken from the pool")
     ap.add_argument("--max-batches", type=int, default=0, help="sweep: at most this many batches per size")
     ap.add_argument("--reps", type=int, default=3, help="sweep: timed steps per batch and layout (median)")
@@ -633,6 +677,9 @@ def main():
     torch.cuda.set_device(0)
     if args.traffic_pass:
         traffic_pass(args)
+        return
+    if args.sweep == "attention-lengths":
+        run_attention_lengths(args)
         return
     if args.sweep:
         run_sweep(args)
