@@ -6,10 +6,11 @@
 // Three launches.  (1) The last hidden row of every prompt (row prompt_kv_off[i+1] - 1 of the
 // unpacked hidden state) is gathered into a [k_pad, d] matrix in the model's dtype, rows past
 // k zero.  (2) One workgroup per 128 vocabulary rows computes their logits for all prompts and
-// reduces them to one (max, lowest id) pair per prompt.  The LM head, vocab x d, is read from
-// HBM exactly once and dominates the traffic: this kernel is HBM-bound on it (2 vocab d bytes
-// in bf16), the prompt matrix being re-read from L2.  (3) One workgroup per prompt reduces the
-// per-workgroup pairs; the order it uses is total, so the result is deterministic.
+// reduces them to one (max, lowest id) pair per prompt.  The LM head, vocab x d, dominates the
+// traffic: it is read from HBM once per pass over the prompts (one pass for up to 128 prompts
+// in bf16), so this kernel is HBM-bound on it (2 vocab d bytes), the prompt matrix being
+// re-read from L2.  (3) One workgroup per prompt reduces the per-workgroup pairs; the order it
+// uses is total, so the result is deterministic.
 #include <math.h>
 
 #include <mutex>
@@ -33,129 +34,183 @@ __device__ __forceinline__ bool better(float av, int ai, float bv, int bi) {
     return av > bv || (av == bv && ai < bi);
 }
 
+// Workgroup (i, j): prompt i's last hidden row, columns 2048 j .. + 2047, 8 per thread (two
+// 16-byte loads); rows k .. k_pad - 1 are zero.  d is a multiple of 8.
 template <typename T>
 __global__ __launch_bounds__(256) void gather_last_kernel(const float* __restrict__ hidden, const int32_t* __restrict__ off,
                                                          int k, int k_pad, int d, T* __restrict__ out) {
-    const int i = blockIdx.x;
-    if (i >= k_pad) return;
-    T* o = out + int64_t(i) * d;
-    if (i >= k) {
-        for (int c = threadIdx.x; c < d; c += blockDim.x) o[c] = static_cast<T>(0.f);
-        return;
+    const int i = blockIdx.x, c = 8 * (blockIdx.y * 256 + threadIdx.x);
+    if (i >= k_pad || c >= d) return;
+    f32x4 a = {}, b = {};
+    if (i < k) {
+        const float* h = hidden + int64_t(off[i + 1] - 1) * d + c;
+        a = *reinterpret_cast<const f32x4*>(h);
+        b = *reinterpret_cast<const f32x4*>(h + 4);
     }
-    const float* h = hidden + int64_t(off[i + 1] - 1) * d;
-    for (int c = threadIdx.x; c < d; c += blockDim.x) o[c] = static_cast<T>(h[c]);
+    T* o = out + int64_t(i) * d + c;
+    if constexpr (sizeof(T) == 2) {
+        bf16x8 v;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) { v[x] = static_cast<bf16>(a[x]); v[4 + x] = static_cast<bf16>(b[x]); }
+        *reinterpret_cast<bf16x8*>(o) = v;
+    } else {
+        *reinterpret_cast<f32x4*>(o) = a;
+        *reinterpret_cast<f32x4*>(o + 4) = b;
+    }
 }
 
-// Wavefront w of workgroup b owns vocabulary rows n0 = 128 b + 32 w .. + 31 (two blocks of
-// 16 on the rows of the 16x16x32 bf16 MFMA) and all prompts, 64 at a time (4 blocks of 16 on
-// its columns).  The weight rows stream from HBM straight into registers: lane l reads 8
-// consecutive K values of row l % 16 at K offset 8 (l / 16) of a 32-wide step, and the
-// fragments of step t + 8 are requested while step t is computed (a ring of 8 steps, 16 KB
-// per wavefront in flight).  Rows past the vocabulary are read as the last row and never
-// reported.  The prompt rows are shared by the 4 wavefronts through LDS, 128 K columns at a
-// time, double-buffered: each 128-column tile is read from L2 once per workgroup.  In block
-// (nb, mb) lane l holds the logits of prompt 16 mb + l % 16 for vocabulary rows
-// n0 + 16 nb + 4 (l / 16) + 0..3.
-constexpr int LM_ROWS = 128;        // vocabulary rows per workgroup
-constexpr int HT = 128;             // K columns per LDS tile of prompt rows
-constexpr int HT_B = 64 * HT * 2;   // one tile: 64 prompt rows x 256 bytes
+// Four wavefronts per workgroup of 128 vocabulary rows: wavefront w owns rows
+// n0 = 128 b + 32 w .. + 31 (two blocks of 16 on the rows of the 16x16x32 bf16 MFMA) and all
+// prompts, 16 MB at a time (MB blocks of 16 on its columns).  K is consumed in chunks of KC
+// columns.  A chunk's weight tile (128 rows x 2 KC bytes) and prompt tile (16 MB rows x 2 KC
+// bytes) go from global memory straight into LDS, each 1 KB load a set of whole row segments,
+// through a ring of NCH chunks: NCH - 1 chunks are in flight while one is consumed.  The LM
+// head streams through once per pass of 16 MB prompts; the prompt rows come from L2.  Rows
+// past the vocabulary or the prompts are read as the last row (every load in range) and never
+// reported.  In block (nb, mb) lane l holds the logits of prompt 16 mb + l % 16 for vocabulary
+// rows n0 + 16 nb + 4 (l / 16) + 0..3.
+constexpr int LM_ROWS = 128;            // vocabulary rows per workgroup
+// Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
+constexpr int kRsrcWord3 = 0x00020000;
+// s_waitcnt immediate: vmcnt(n) and lgkmcnt(0), expcnt not waited for (gfx9 encoding).
+constexpr int wait_vm_lgkm0(int n) { return ((n >> 4) << 14) | (n & 15) | 0x0070; }
 
-// LDS swizzle of the prompt tile: row r's 16-byte chunk q sits at q ^ g(r), g built from r's
-// bits 0, 1, 2 placed at bits 0, 2, 3.  A fragment read serves lanes i and i + 32 together:
-// rows r..r+7 at chunks q and q ^ 2; a 256-byte row spans all 64 banks, so those 16 accesses
-// are conflict-free when the g(r) fall in distinct classes {x, x ^ 2}, which this g does.
-__device__ __forceinline__ int gsw(int r) { return (r & 1) | (((r >> 1) & 1) << 2) | (((r >> 2) & 1) << 3); }
+typedef __attribute__((address_space(3))) void lds_void;
 
-__global__ __launch_bounds__(256) void lm_head_bf16_kernel(const bf16* __restrict__ hl, int k, int k_pad,
-                                                           const bf16* __restrict__ W, int V, int d,
-                                                           float* __restrict__ logits, ArgMax* __restrict__ part) {
-    __shared__ __attribute__((aligned(16))) char tile[2][HT_B];
-    __shared__ ArgMax red[4][64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n0 = blockIdx.x * LM_ROWS + wave * 32;
-    const int lr = lane & 15, q4 = lane >> 4;
-    const bf16* wrow[2];
+// LDS swizzles: logical 16-byte chunk c of tile row r sits at c ^ f(r).  A fragment read takes
+// chunk 4 s + l / 16 of rows l % 16, and the LDS serves lanes i and i + 32 together: 8 rows x
+// chunks {c, c ^ 2}.
+// 128-byte rows (KC = 64; a row covers half the banks): f's bits are r's bits 1, 3 and 2, so the
+// 16 (r % 2, physical chunk) pairs are distinct.
+// 256-byte rows (KC = 128; a row covers all 64 banks): f's bits 0, 2, 3 are r's bits 0, 1, 2, so
+// the 8 rows fall in distinct classes {x, x ^ 2} and the 16 physical chunks are distinct.
+template <int KC>
+__device__ __forceinline__ int lm_swz(int r) {
+    if constexpr (KC == 64) return ((r >> 1) & 1) | (((r >> 3) & 1) << 1) | (r & 4);
+    else return (r & 1) | (((r >> 1) & 1) << 2) | (((r >> 2) & 1) << 3);
+}
+
+template <int MB, int KC, int NCH>
+struct LmGeom {
+    static constexpr int ROW_B = 2 * KC;                // bytes of a tile row
+    static constexpr int CPR = ROW_B / 16;              // 16-byte chunks per row
+    static constexpr int RPL = 1024 / ROW_B;            // rows per 1 KB load
+    static constexpr int W_B = LM_ROWS * ROW_B;         // weight tile of a chunk
+    static constexpr int P_B = 16 * MB * ROW_B;         // prompt tile of a chunk
+    static constexpr int CH_B = W_B + P_B;
+    static constexpr int W_LD = W_B / 1024 / 4;         // 1 KB loads per wavefront per chunk
+    static constexpr int P_LD = P_B / 1024 / 4;
+    static constexpr int LDS = NCH * CH_B;
+    static_assert(KC == 64 || KC == 128, "tile rows of 128 or 256 bytes");
+    static_assert(P_LD >= 1 && LDS + 4 * 16 * MB * 8 <= 160 * 1024, "LDS of one workgroup");
+    static_assert((NCH - 2) * (W_LD + P_LD) <= 63, "vmcnt range");
+};
+
+// The loads of wavefront `wave` for K columns of chunk c (clamped: always in range) into ring
+// slot c % NCH.
+template <class G, int NCH>
+__device__ __forceinline__ void lm_issue(__amdgpu_buffer_rsrc_t wrs, __amdgpu_buffer_rsrc_t hrs, char* smem, int c,
+                                         int n_ch, int wave, const int* woff, const int* poff) {
+    const int col_b = min(c, n_ch - 1) * G::ROW_B;
+    char* slot = smem + (c % NCH) * G::CH_B;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) wrow[nb] = W + int64_t(min(n0 + 16 * nb + lr, V - 1)) * d + 8 * q4;
-    const int S = d / 32;               // K steps of 32; d % 256 == 0, so S % 8 == 0
-    const int n_tiles = d / HT;
-    // prompt-tile loads: load t (0..3) of wavefront w covers rows 4 (4 w + t) + l / 16, chunk l % 16
-    int h_row[4], h_lds[4];
+    for (int t = 0; t < G::W_LD; ++t)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, (lds_void*)(slot + (G::W_LD * wave + t) * 1024), 16, woff[t],
+                                                 col_b, 0, 0);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        h_row[t] = 4 * (4 * wave + t) + q4;
-        h_lds[t] = h_row[t] * 256 + 16 * (lr ^ gsw(h_row[t] & 7));
+    for (int t = 0; t < G::P_LD; ++t)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(hrs, (lds_void*)(slot + G::W_B + (G::P_LD * wave + t) * 1024), 16,
+                                                 poff[t], col_b, 0, 0);
+}
+
+template <int MB, int KC, int NCH, int WR>
+__global__ __launch_bounds__(256, 1) void lm_head_bf16_kernel(const bf16* __restrict__ hl, int k, int k_pad,
+                                                              const bf16* __restrict__ W, int V, int d,
+                                                              float* __restrict__ logits,
+                                                              ArgMax* __restrict__ part) {
+    using G = LmGeom<MB, KC, NCH>;
+    constexpr int NB = LM_ROWS / WR / 16;   // row blocks of a wavefront
+    constexpr int MW = MB * WR / 4;         // prompt blocks of a wavefront
+    static_assert(NB * MW * 4 == 8 * MB, "the 4 wavefronts tile 128 rows x 16 MB prompts");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ ArgMax red[WR][16 * MB];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wr = wave % WR, wp = wave / WR;
+    const int nb0 = blockIdx.x * LM_ROWS;
+    const int n0 = nb0 + wr * 16 * NB;
+    const int lr = lane & 15, q4 = lane >> 4, lrow = lane / G::CPR, lchk = lane % G::CPR;
+    const int n_ch = d / KC;
+    const int last_row = min(V - 1 - nb0, LM_ROWS - 1);   // rows past it (vocabulary end) read it again
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>(W + int64_t(nb0) * d), 0, (last_row + 1) * d * 2, kRsrcWord3);
+    // load t of wavefront w fills rows RPL (W_LD w + t) + l / CPR of the weight tile (rows
+    // RPL (P_LD w + t) + l / CPR of the prompt tile); lane l lands at physical chunk l % CPR and
+    // fetches the logical chunk that the swizzle puts there
+    int woff[G::W_LD];
+#pragma unroll
+    for (int t = 0; t < G::W_LD; ++t) {
+        const int row = G::RPL * (G::W_LD * wave + t) + lrow;
+        woff[t] = min(row, last_row) * d * 2 + 16 * (lchk ^ lm_swz<KC>(row));
     }
-    // fragment reads: row 16 mb + lr, chunk 4 s + q4 (s = step within the tile)
-    const int f_base = lr * 256;
-    const int f_sw = gsw(lr & 7);
-    for (int m0 = 0; m0 < k_pad; m0 += 64) {
-        const int nmb = min(4, (k_pad - m0) / 16);
-        bf16x8 hreg[4];
-        auto load_tile = [&](int c) {   // prompt rows m0.., K columns c*HT.. (clamped: always in range)
-            const int cc = min(c, n_tiles - 1);
+    const int f_sw = lm_swz<KC>(lr);
+    for (int m0 = 0; m0 < k_pad; m0 += 16 * MB) {
+        const int nmb = min(MB, (k_pad - m0) / 16);
+        const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<bf16*>(hl + int64_t(m0) * d), 0, 16 * nmb * d * 2, kRsrcWord3);
+        int poff[G::P_LD];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int row = min(m0 + h_row[t], k_pad - 1);
-                hreg[t] = *reinterpret_cast<const bf16x8*>(hl + int64_t(row) * d + cc * HT + lr * 8);
-            }
-        };
-        auto store_tile = [&](int buf) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) *reinterpret_cast<bf16x8*>(tile[buf] + h_lds[t]) = hreg[t];
-        };
-        bf16x8 ring[8][2];
-        auto load_w = [&](int u, int t) {   // weight fragments of step t (clamped) into ring slot u
-            const int tt = min(t, S - 1);
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) ring[u][nb] = *reinterpret_cast<const bf16x8*>(wrow[nb] + 32 * tt);
-        };
-        f32x4 acc[2][4] = {};
-        auto step = [&](int u, int buf, int s) {   // compute ring slot u with tile buf, step s of it
-#pragma unroll
-            for (int mb = 0; mb < 4; ++mb) {
-                if (mb >= nmb) break;
-                const bf16x8 h = *reinterpret_cast<const bf16x8*>(
-                    tile[buf] + f_base + 16 * mb * 256 + 16 * ((4 * s + q4) ^ f_sw));
-#pragma unroll
-                for (int nb = 0; nb < 2; ++nb)
-                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[u][nb], h, acc[nb][mb], 0, 0, 0);
-            }
-        };
-        load_tile(0);
-        store_tile(0);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) load_w(u, u);
-        __syncthreads();
-        for (int t0 = 0; t0 < S; t0 += 8) {
-            const int c = t0 / 4;   // tiles c (buffer 0) and c + 1 (buffer 1)
-            load_tile(c + 1);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                step(u, 0, u);
-                load_w(u, t0 + 8 + u);
-            }
-            store_tile(1);
-            __syncthreads();
-            load_tile(c + 2);
-#pragma unroll
-            for (int u = 4; u < 8; ++u) {
-                step(u, 1, u - 4);
-                load_w(u, t0 + 8 + u);
-            }
-            store_tile(0);
-            __syncthreads();
+        for (int t = 0; t < G::P_LD; ++t) {
+            const int row = G::RPL * (G::P_LD * wave + t) + lrow;
+            poff[t] = min(row, 16 * nmb - 1) * d * 2 + 16 * (lchk ^ lm_swz<KC>(row));
         }
-        // logits and each lane's best of its 8 vocabulary rows, per prompt block
+        f32x4 acc[NB][MW] = {};
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-            if (mb >= nmb) break;
-            const int m = m0 + 16 * mb + lr;
+        for (int c = 0; c < NCH - 1; ++c) lm_issue<G, NCH>(wrs, hrs, smem, c, n_ch, wave, woff, poff);
+        // At the top of chunk c the loads issued after its own are those of chunks c + 1 ..
+        // c + NCH - 2: (NCH - 2) chunks of W_LD + P_LD loads per wavefront.
+        for (int c = 0; c < n_ch; ++c) {
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((NCH - 2) * (G::W_LD + G::P_LD)));
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            // into the slot every wavefront finished at c - 1
+            lm_issue<G, NCH>(wrs, hrs, smem, c + NCH - 1, n_ch, wave, woff, poff);
+            const char* slot = smem + (c % NCH) * G::CH_B;
+#pragma unroll
+            for (int st = 0; st < KC / 32; ++st) {
+                const int ch = 16 * ((4 * st + q4) ^ f_sw);
+                bf16x8 wf[NB], pf[MW];
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    wf[nb] = *reinterpret_cast<const bf16x8*>(slot + (n0 - nb0 + 16 * nb + lr) * G::ROW_B + ch);
+#pragma unroll
+                for (int mb = 0; mb < MW; ++mb)
+                    if (MW * wp + mb < nmb)
+                        pf[mb] = *reinterpret_cast<const bf16x8*>(slot + G::W_B + (16 * (MW * wp + mb) + lr) * G::ROW_B + ch);
+#pragma unroll
+                for (int mb = 0; mb < MW; ++mb) {
+                    if (MW * wp + mb >= nmb) break;
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb)
+                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[nb], pf[mb], acc[nb][mb], 0, 0, 0);
+                }
+            }
+        }
+        // the loads past the last chunk are dead (clamped, never read); none may still be writing
+        // LDS when the ring is refilled or the workgroup ends
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+        // logits and each lane's best of its 4 NB vocabulary rows, per prompt block
+#pragma unroll
+        for (int mb = 0; mb < MW; ++mb) {
+            const int gb = MW * wp + mb;
+            if (gb >= nmb) break;
+            const int m = m0 + 16 * gb + lr;
             float bv = -INFINITY;
             int bi = INT32_MAX;
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < NB; ++nb) {
                 const int nbase = n0 + 16 * nb + 4 * q4;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -172,18 +227,18 @@ __global__ __launch_bounds__(256) void lm_head_bf16_kernel(const bf16* __restric
                 const int oi = __shfl_xor(bi, x);
                 if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
             }
-            if (lane < 16) red[wave][16 * mb + lane] = ArgMax{bv, bi};
+            if (lane < 16) red[wr][16 * gb + lane] = ArgMax{bv, bi};
         }
         __syncthreads();
-        // wavefront 0 combines the 4 wavefronts' rows for the 64 prompts
-        if (wave == 0 && lane < 16 * nmb && m0 + lane < k) {
-            ArgMax b = red[0][lane];
+        // the WR row groups combined for the 16 MB prompts; prompt m's pairs are contiguous
+        if (threadIdx.x < 16 * nmb && m0 + threadIdx.x < k) {
+            ArgMax b = red[0][threadIdx.x];
 #pragma unroll
-            for (int w2 = 1; w2 < 4; ++w2) {
-                const ArgMax o = red[w2][lane];
+            for (int w2 = 1; w2 < WR; ++w2) {
+                const ArgMax o = red[w2][threadIdx.x];
                 if (better(o.v, o.i, b.v, b.i)) b = o;
             }
-            part[int64_t(blockIdx.x) * k + m0 + lane] = b;
+            part[int64_t(m0 + threadIdx.x) * gridDim.x + blockIdx.x] = b;
         }
         __syncthreads();
     }
@@ -203,7 +258,7 @@ __global__ __launch_bounds__(64) void lm_head_f32_kernel(const float* __restrict
         s = wave_sum(s);
         if (lane == 0) {
             if (logits) logits[int64_t(m) * V + n] = s;
-            part[int64_t(n) * k + m] = ArgMax{s, n};   // a NaN logit never wins the final reduction
+            part[int64_t(m) * V + n] = ArgMax{s, n};   // a NaN logit never wins the final reduction
         }
     }
 }
@@ -218,7 +273,7 @@ __global__ __launch_bounds__(256) void argmax_finalize_kernel(const ArgMax* __re
     const int m = blockIdx.x;
     ArgMax b{-INFINITY, INT32_MAX};
     for (int j = threadIdx.x; j < n_blocks; j += blockDim.x) {
-        const ArgMax o = part[int64_t(j) * k + m];
+        const ArgMax o = part[int64_t(m) * n_blocks + j];
         if (better(o.v, o.i, b.v, b.i)) b = o;
     }
 #pragma unroll
@@ -235,6 +290,19 @@ __global__ __launch_bounds__(256) void argmax_finalize_kernel(const ArgMax* __re
             if (better(red[w].v, red[w].i, b.v, b.i)) b = red[w];
         tokens[m] = b.i == INT32_MAX ? -1 : b.i;   // -1: every logit was NaN
     }
+}
+
+template <int MB, int KC, int NCH, int WR>
+void lm_head_launch(const bf16* hl, int k, int k_pad, const bf16* W, int V, int d, float* logits, ArgMax* part,
+                    int n_blocks, hipStream_t s) {
+    constexpr int lds = LmGeom<MB, KC, NCH>::LDS;
+    static bool attr = [] {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&lm_head_bf16_kernel<MB, KC, NCH, WR>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        return true;
+    }();
+    (void)attr;
+    lm_head_bf16_kernel<MB, KC, NCH, WR><<<n_blocks, 256, lds, s>>>(hl, k, k_pad, W, V, d, logits, part);
 }
 
 }  // namespace
@@ -281,14 +349,17 @@ void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, i
     char* ws = static_cast<char*>(workspace);
     ArgMax* part = reinterpret_cast<ArgMax*>(ws + (size_t(k_pad) * d * e + 255) / 256 * 256);
     const int n_blocks = (V + (dtype == PP_BF16 ? LM_ROWS : VB) - 1) / (dtype == PP_BF16 ? LM_ROWS : VB);
+    const dim3 g_grid(k_pad, (d + 2047) / 2048);
     if (dtype == PP_BF16) {
         bf16* hl = reinterpret_cast<bf16*>(ws);
-        gather_last_kernel<bf16><<<k_pad, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);
-        lm_head_bf16_kernel<<<n_blocks, 256, 0, s>>>(hl, k, k_pad, static_cast<const bf16*>(lm_head), V, d, logits,
-                                                     part);
+        gather_last_kernel<bf16><<<g_grid, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);
+        if (k_pad <= 64)
+            lm_head_launch<4, 64, 4, 2>(hl, k, k_pad, static_cast<const bf16*>(lm_head), V, d, logits, part, n_blocks, s);
+        else
+            lm_head_launch<8, 64, 4, 2>(hl, k, k_pad, static_cast<const bf16*>(lm_head), V, d, logits, part, n_blocks, s);
     } else {
         float* hl = reinterpret_cast<float*>(ws);
-        gather_last_kernel<float><<<k_pad, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);
+        gather_last_kernel<float><<<g_grid, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);
         lm_head_f32_kernel<<<n_blocks, 64, 0, s>>>(hl, k, static_cast<const float*>(lm_head), V, d, logits, part);
     }
     argmax_finalize_kernel<<<k, 256, 0, s>>>(part, n_blocks, k, tokens);

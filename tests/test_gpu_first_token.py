@@ -67,18 +67,25 @@ def _check(lengths, hidden, lm_head, tokens, logits, bf16=True):
             assert 0 <= t < lm_head.shape[0] and ref[i, t] >= top[0] - slack, f"prompt {i}: token {t} not a maximum"
 
 
-@pytest.mark.parametrize("case", ["one-prompt", "ragged-vocab", "two-prompt-chunks", "llama2-7b-vocab"])
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("case", ["one-prompt", "ragged-vocab", "two-prompt-chunks", "two-passes-of-128",
+                                  "llama2-7b-vocab", "bimodal-96-prompts", "llama3-8b-vocab"])
 def test_first_token_bf16(case):
-    if case == "llama2-7b-vocab":
-        # full size: the 64 prompts of the Llama-2-7B lognormal workload, vocab 32000, d 4096
-        lengths = W.draw_lengths(W.workload(2), 0)
-        V, d = 32000, 4096
+    # up to 64 prompts are one pass of 64; more, passes of 128 (the last one partial)
+    if case in ("llama2-7b-vocab", "bimodal-96-prompts", "llama3-8b-vocab"):
+        # full size: the prompts of the Llama-2-7B lognormal (64), bimodal (96) and Llama-3-8B (128)
+        # workloads with their vocabularies, d 4096
+        wl, V = {"llama2-7b-vocab": (2, 32000), "bimodal-96-prompts": (3, 32000), "llama3-8b-vocab": (4, 128256)}[case]
+        lengths = W.draw_lengths(W.workload(wl), 0)
+        d = 4096
     else:
         lengths = {"one-prompt": [37], "ragged-vocab": [5, 1, 12, 3, 9],
-                   "two-prompt-chunks": list(np.random.default_rng(3).integers(1, 40, 70))}[case]
-        V, d = {"one-prompt": (1000, 256), "ragged-vocab": (1000, 256), "two-prompt-chunks": (3000, 512)}[case]
+                   "two-prompt-chunks": list(np.random.default_rng(3).integers(1, 40, 70)),
+                   "two-passes-of-128": list(np.random.default_rng(4).integers(1, 30, 150))}[case]
+        V, d = {"one-prompt": (1000, 256), "ragged-vocab": (1000, 256), "two-prompt-chunks": (3000, 512),
+                "two-passes-of-128": (2000, 256)}[case]
     rng = np.random.default_rng([len(lengths), V, d])
-    hidden = rng.standard_normal((int(np.sum(lengths)), d)).astype(np.float32)   # unit RMS, like a normed state
+    hidden = rng.standard_normal((int(np.sum(lengths)), d), dtype=np.float32)   # unit RMS, like a normed state
     lm_head = rand_bf16(rng, (V, d), 0.02)
     tokens, logits = _run(lengths, hidden, lm_head)
     _check(lengths, hidden, lm_head, tokens, logits)
