@@ -244,6 +244,193 @@ __global__ __launch_bounds__(256, 1) void lm_head_bf16_kernel(const bf16* __rest
     }
 }
 
+// Up to 64 prompts, d a multiple of 512: the same workgroup tile (128 vocabulary rows x 64
+// prompts) with the LM head streamed as long row segments.  Chunk (s, rb) of a workgroup is
+// 16 vocabulary rows x 512 K columns, one whole 1 KB segment of each row per load; chunks go
+// segment-major (s = 0, 1, ..; rb = 0..7 within a segment) through an LDS ring of NW chunks.
+// Cache-cold, HBM streams these 1 KB segments markedly faster than 128-byte ones spread over
+// 128 rows.  The wavefronts split K instead of rows: wavefront w takes columns 128 w .. + 127 of
+// every chunk (4 MFMA K-steps) and accumulates all 8 row blocks x 4 prompt blocks over its
+// quarter of K.  The prompt tile of segment s (64 rows x 1 KB) sits in LDS; at the segment's
+// first chunk each wavefront moves its quarter into registers (16 fragments), after which the
+// tile of segment s + 1 is loaded in its place, a quarter with each of the segment's first 4
+// chunks.  At the end the 4 partial sums of each logit are added through LDS in wavefront
+// order.
+constexpr int SEG_COLS = 512;                 // K columns of a chunk
+constexpr int SEG_W_B = 16 * SEG_COLS * 2;    // 16 KB of weights per chunk
+constexpr int SEG_P_B = 64 * SEG_COLS * 2;    // 64 KB prompt tile of a segment
+
+// s_waitcnt count at chunk rb of a segment: the loads a wavefront issued after the one of the
+// awaited chunk.  Each chunk step issues the chunk NW - 1 ahead (4 loads) and then, at rb < 4, a
+// quarter of the next prompt tile (4 loads); chunk rb was issued NW - 1 steps earlier.  Steps
+// before the first chunk are the prologue (weights only, the first prompt tile before them),
+// which is what rb < 0 reads as (rb 4..7 carry no prompt loads) while NW <= 5.
+constexpr int seg_p_loads(int rb) { return ((rb % 8 + 8) % 8) < 4 ? 4 : 0; }
+constexpr int seg_wait(int rb, int NW) {
+    int n = seg_p_loads(rb - NW + 1);
+    for (int j = rb - NW + 2; j <= rb - 1; ++j) n += 4 + seg_p_loads(j);
+    return n;
+}
+
+static_assert(seg_wait(0, 4) == 8 && seg_wait(1, 4) == 12 && seg_wait(3, 4) == 20 && seg_wait(4, 4) == 20 &&
+                  seg_wait(7, 4) == 8 && seg_wait(0, 5) == 12 && seg_wait(4, 5) == 28 && seg_wait(7, 5) == 16,
+              "wait counts worked out by hand for rings of 4 and 5 chunks");
+
+// s_waitcnt needs an immediate: rb is a constant of the unrolled chunk loop, so the switch folds.
+template <int NW>
+__device__ __forceinline__ void seg_waitcnt(int rb) {
+    switch (rb) {
+        case 0: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(0, NW))); break;
+        case 1: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(1, NW))); break;
+        case 2: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(2, NW))); break;
+        case 3: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(3, NW))); break;
+        case 4: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(4, NW))); break;
+        case 5: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(5, NW))); break;
+        case 6: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(6, NW))); break;
+        default: __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(seg_wait(7, NW))); break;
+    }
+}
+
+template <int NW>
+__global__ __launch_bounds__(256, 1) void lm_head_seg_kernel(const bf16* __restrict__ hl, int k, int k_pad,
+                                                             const bf16* __restrict__ W, int V, int d,
+                                                             float* __restrict__ logits, ArgMax* __restrict__ part) {
+    static_assert(NW >= 2 && NW <= 5, "the prologue reading of seg_wait");
+    static_assert(NW * SEG_W_B + SEG_P_B <= 144 * 1024 && 4 * 8 * 4 * 64 * 16 <= NW * SEG_W_B + SEG_P_B, "LDS");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ ArgMax red[4][64];
+    char* const pbuf = smem + NW * SEG_W_B;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int nb0 = blockIdx.x * LM_ROWS;
+    const int lr = lane & 15, q4 = lane >> 4;
+    const int n_seg = d / SEG_COLS;
+    const int rows_p = k_pad;                                  // prompt rows present (<= 64)
+    const int last_row = min(V - 1 - nb0, LM_ROWS - 1);
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>(W + int64_t(nb0) * d), 0, (last_row + 1) * d * 2, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(hl), 0, rows_p * d * 2,
+                                                                         kRsrcWord3);
+    // 1 KB row segments land with lane l at physical 16-byte chunk l and take the logical chunk
+    // l ^ f(r) (lm_swz<128>: within each 256-byte bank window, so fragment reads of 8 rows x
+    // chunks {c, c ^ 2} hit 16 distinct bank groups)
+    auto w_issue = [&](int g) {       // chunk g (clamped: dead chunks re-read the last) -> slot g % NW
+        const int gc = min(g, 8 * n_seg - 1), sg = gc >> 3, rb = gc & 7;
+        char* slot = smem + (g % NW) * SEG_W_B;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int r = 4 * wave + t;
+            const int soff = min(16 * rb + r, last_row) * d * 2 + sg * SEG_COLS * 2;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, (lds_void*)(slot + r * 1024), 16,
+                                                     16 * (lane ^ lm_swz<128>(r)), soff, 0, 0);
+        }
+    };
+    auto p_issue = [&](int sg, int i) {   // quarter i of the prompt tile of segment sg (clamped)
+        const int sc = min(sg, n_seg - 1);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int r = 16 * wave + 4 * i + t;
+            const int soff = min(r, rows_p - 1) * d * 2 + sc * SEG_COLS * 2;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(hrs, (lds_void*)(pbuf + r * 1024), 16,
+                                                     16 * (lane ^ lm_swz<128>(r)), soff, 0, 0);
+        }
+    };
+    f32x4 acc[8][4] = {};
+    bf16x8 pf[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p_issue(0, i);
+#pragma unroll
+    for (int g = 0; g < NW - 1; ++g) w_issue(g);
+    for (int sg = 0; sg < n_seg; ++sg) {
+#pragma unroll
+        for (int rb = 0; rb < 8; ++rb) {
+            const int g = 8 * sg + rb;
+            __builtin_amdgcn_sched_barrier(0);
+            seg_waitcnt<NW>(rb);
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            if (rb == 0) {
+                // this wavefront's quarter of the segment's prompt tile into registers; then the
+                // buffer is free for the next segment's tile
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+#pragma unroll
+                    for (int mb = 0; mb < 4; ++mb) {
+                        const int r = 16 * mb + lr;
+                        pf[st][mb] = *reinterpret_cast<const bf16x8*>(
+                            pbuf + r * 1024 + 16 * ((16 * wave + 4 * st + q4) ^ lm_swz<128>(r)));
+                    }
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(63));
+                __builtin_amdgcn_s_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            w_issue(g + NW - 1);
+            if (rb < 4) p_issue(sg + 1, rb);
+            const char* slot = smem + (g % NW) * SEG_W_B;
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const bf16x8 wf = *reinterpret_cast<const bf16x8*>(
+                    slot + lr * 1024 + 16 * ((16 * wave + 4 * st + q4) ^ lm_swz<128>(lr)));
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
+                    acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, pf[st][mb], acc[rb][mb], 0, 0, 0);
+            }
+        }
+    }
+    // every load (the dead ones past the last chunk included) has landed before LDS is reused
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+    __syncthreads();
+    f32x4* part_sum = reinterpret_cast<f32x4*>(smem);      // [wave][rb][mb][lane]
+#pragma unroll
+    for (int rb = 0; rb < 8; ++rb)
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) part_sum[((wave * 8 + rb) * 4 + mb) * 64 + lane] = acc[rb][mb];
+    __syncthreads();
+    // wavefront w finishes row blocks 2 w and 2 w + 1: rows nb0 + 32 w + 16 nb + 4 (l / 16) + 0..3
+    const int n0 = nb0 + 32 * wave;
+    const int nmb = k_pad / 16;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+        if (mb >= nmb) break;
+        const int m = 16 * mb + lr;
+        float bv = -INFINITY;
+        int bi = INT32_MAX;
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const int rb = 2 * wave + nb;
+            f32x4 v = part_sum[((0 * 8 + rb) * 4 + mb) * 64 + lane];
+#pragma unroll
+            for (int w2 = 1; w2 < 4; ++w2) v += part_sum[((w2 * 8 + rb) * 4 + mb) * 64 + lane];
+            const int nbase = n0 + 16 * nb + 4 * q4;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                if (nbase + r >= V) continue;
+                if (logits && m < k) logits[int64_t(m) * V + nbase + r] = v[r];
+                if (better(v[r], nbase + r, bv, bi)) { bv = v[r]; bi = nbase + r; }
+            }
+        }
+#pragma unroll
+        for (int x = 16; x < 64; x <<= 1) {
+            const float ov = __shfl_xor(bv, x);
+            const int oi = __shfl_xor(bi, x);
+            if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+        }
+        if (lane < 16) red[wave][16 * mb + lane] = ArgMax{bv, bi};
+    }
+    __syncthreads();
+    if (threadIdx.x < k_pad && threadIdx.x < k) {
+        ArgMax b = red[0][threadIdx.x];
+#pragma unroll
+        for (int w2 = 1; w2 < 4; ++w2) {
+            const ArgMax o = red[w2][threadIdx.x];
+            if (better(o.v, o.i, b.v, b.i)) b = o;
+        }
+        part[int64_t(threadIdx.x) * gridDim.x + blockIdx.x] = b;
+    }
+}
+
 // float32 model: one wavefront per vocabulary row (its lanes split d, the row read once,
 // coalesced), every prompt's logit reduced across the wavefront in a fixed order.
 __global__ __launch_bounds__(64) void lm_head_f32_kernel(const float* __restrict__ hl, int k, const float* __restrict__ W,
@@ -305,6 +492,19 @@ void lm_head_launch(const bf16* hl, int k, int k_pad, const bf16* W, int V, int 
     lm_head_bf16_kernel<MB, KC, NCH, WR><<<n_blocks, 256, lds, s>>>(hl, k, k_pad, W, V, d, logits, part);
 }
 
+template <int NW>
+void lm_head_seg_launch(const bf16* hl, int k, int k_pad, const bf16* W, int V, int d, float* logits, ArgMax* part,
+                        int n_blocks, hipStream_t s) {
+    constexpr int lds = NW * SEG_W_B + SEG_P_B;
+    static bool attr = [] {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&lm_head_seg_kernel<NW>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        return true;
+    }();
+    (void)attr;
+    lm_head_seg_kernel<NW><<<n_blocks, 256, lds, s>>>(hl, k, k_pad, W, V, d, logits, part);
+}
+
 }  // namespace
 
 // Workspace of pp_first_token_noalloc: a file-scope array of this code object, one copy per
@@ -353,7 +553,9 @@ void first_token(int dtype, const float* hidden, const int32_t* prompt_kv_off, i
     if (dtype == PP_BF16) {
         bf16* hl = reinterpret_cast<bf16*>(ws);
         gather_last_kernel<bf16><<<g_grid, 256, 0, s>>>(hidden, prompt_kv_off, k, k_pad, d, hl);
-        if (k_pad <= 64)
+        if (k_pad <= 64 && d % SEG_COLS == 0)
+            lm_head_seg_launch<4>(hl, k, k_pad, static_cast<const bf16*>(lm_head), V, d, logits, part, n_blocks, s);
+        else if (k_pad <= 64)
             lm_head_launch<4, 64, 4, 2>(hl, k, k_pad, static_cast<const bf16*>(lm_head), V, d, logits, part, n_blocks, s);
         else
             lm_head_launch<8, 64, 4, 2>(hl, k, k_pad, static_cast<const bf16*>(lm_head), V, d, logits, part, n_blocks, s);

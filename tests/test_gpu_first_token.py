@@ -68,10 +68,12 @@ def _check(lengths, hidden, lm_head, tokens, logits, bf16=True):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("case", ["one-prompt", "ragged-vocab", "two-prompt-chunks", "two-passes-of-128",
-                                  "llama2-7b-vocab", "bimodal-96-prompts", "llama3-8b-vocab"])
+@pytest.mark.parametrize("case", ["one-prompt", "ragged-vocab", "ragged-vocab-d512", "33-prompts-d1024",
+                                  "two-prompt-chunks", "two-passes-of-128", "llama2-7b-vocab", "bimodal-96-prompts",
+                                  "llama3-8b-vocab"])
 def test_first_token_bf16(case):
-    # up to 64 prompts are one pass of 64; more, passes of 128 (the last one partial)
+    # up to 64 prompts are one pass of 64 (K in segments of 512 columns when d allows); more,
+    # passes of 128 (the last one partial)
     if case in ("llama2-7b-vocab", "bimodal-96-prompts", "llama3-8b-vocab"):
         # full size: the prompts of the Llama-2-7B lognormal (64), bimodal (96) and Llama-3-8B (128)
         # workloads with their vocabularies, d 4096
@@ -79,10 +81,12 @@ def test_first_token_bf16(case):
         lengths = W.draw_lengths(W.workload(wl), 0)
         d = 4096
     else:
-        lengths = {"one-prompt": [37], "ragged-vocab": [5, 1, 12, 3, 9],
+        lengths = {"one-prompt": [37], "ragged-vocab": [5, 1, 12, 3, 9], "ragged-vocab-d512": [5, 1, 12, 3, 9],
+                   "33-prompts-d1024": list(np.random.default_rng(5).integers(1, 50, 33)),
                    "two-prompt-chunks": list(np.random.default_rng(3).integers(1, 40, 70)),
                    "two-passes-of-128": list(np.random.default_rng(4).integers(1, 30, 150))}[case]
-        V, d = {"one-prompt": (1000, 256), "ragged-vocab": (1000, 256), "two-prompt-chunks": (3000, 512),
+        V, d = {"one-prompt": (1000, 256), "ragged-vocab": (1000, 256), "ragged-vocab-d512": (1000, 512),
+                "33-prompts-d1024": (777, 1024), "two-prompt-chunks": (3000, 512),
                 "two-passes-of-128": (2000, 256)}[case]
     rng = np.random.default_rng([len(lengths), V, d])
     hidden = rng.standard_normal((int(np.sum(lengths)), d), dtype=np.float32)   # unit RMS, like a normed state
@@ -102,10 +106,11 @@ def test_first_token_bf16_without_logits_matches_with():
     _check(lengths, hidden, lm_head, t1, logits)
 
 
-def test_first_token_ties_go_to_the_lowest_id_and_nan_gives_minus_one():
+@pytest.mark.parametrize("d", [256, 512])
+def test_first_token_ties_go_to_the_lowest_id_and_nan_gives_minus_one(d):
     rng = np.random.default_rng(12)
     lengths = [3, 5, 2]                          # last rows 2, 7, 9
-    d, V = 256, 1000
+    V = 1000
     hidden = rng.standard_normal((10, d)).astype(np.float32)
     lm_head = rand_bf16(rng, (V, d), 0.02)
     hb = D.round_bf16(hidden[2].astype(np.float64))
