@@ -332,8 +332,26 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
             float mm = -INFINITY, ll = 0.f, o[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) o[e] = 0.f;
-            for (int c = 0; c < nc + ng; ++c) {
-                const float* pp = base + int64_t(c < nc ? c : ac.n_ctx_chunks + c - nc) * PS;
+            // chunks merged in order; the loads of 4 chunks are issued together so that a long
+            // prompt waits for one L2 round trip per 4 chunks, not per chunk (8: more registers,
+            // fewer waves, slower)
+            const int n = nc + ng;
+            auto chunk = [&](int c) { return base + int64_t(c < nc ? c : ac.n_ctx_chunks + c - nc) * PS; };
+            int c = 0;
+            for (; c + 4 <= n; c += 4) {
+                float o2[4][8], m2[4], l2[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const float* pp = chunk(c + u);
+                    load8(pp + ch * 8, o2[u]);
+                    m2[u] = pp[128];
+                    l2[u] = pp[129];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) merge<8>(mm, ll, o, m2[u], l2[u], o2[u]);
+            }
+            for (; c < n; ++c) {
+                const float* pp = chunk(c);
                 float o2[8];
                 load8(pp + ch * 8, o2);
                 merge<8>(mm, ll, o, pp[128], pp[129], o2);
