@@ -68,7 +68,7 @@ def _check(lengths, hidden, lm_head, tokens, logits, bf16=True):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("case", ["one-prompt", "ragged-vocab", "ragged-vocab-d512", "33-prompts-d1024",
+@pytest.mark.parametrize("case", ["one-prompt", "one-prompt-d512", "ragged-vocab", "ragged-vocab-d512", "33-prompts-d1024",
                                   "two-prompt-chunks", "two-passes-of-128", "llama2-7b-vocab", "bimodal-96-prompts",
                                   "llama3-8b-vocab"])
 def test_first_token_bf16(case):
@@ -81,11 +81,13 @@ def test_first_token_bf16(case):
         lengths = W.draw_lengths(W.workload(wl), 0)
         d = 4096
     else:
-        lengths = {"one-prompt": [37], "ragged-vocab": [5, 1, 12, 3, 9], "ragged-vocab-d512": [5, 1, 12, 3, 9],
+        lengths = {"one-prompt": [37], "one-prompt-d512": [1], "ragged-vocab": [5, 1, 12, 3, 9],
+                   "ragged-vocab-d512": [5, 1, 12, 3, 9],
                    "33-prompts-d1024": list(np.random.default_rng(5).integers(1, 50, 33)),
                    "two-prompt-chunks": list(np.random.default_rng(3).integers(1, 40, 70)),
                    "two-passes-of-128": list(np.random.default_rng(4).integers(1, 30, 150))}[case]
-        V, d = {"one-prompt": (1000, 256), "ragged-vocab": (1000, 256), "ragged-vocab-d512": (1000, 512),
+        V, d = {"one-prompt": (1000, 256), "one-prompt-d512": (129, 512), "ragged-vocab": (1000, 256),
+                "ragged-vocab-d512": (1000, 512),
                 "33-prompts-d1024": (777, 1024), "two-prompt-chunks": (3000, 512),
                 "two-passes-of-128": (2000, 256)}[case]
     rng = np.random.default_rng([len(lengths), V, d])
