@@ -101,6 +101,29 @@ def test_bf16_layer_shapes_vs_oracle(wid, n_layers, lengths, cap):
     _gate(name, errs, floor)
 
 
+# Widths that are not powers of two, on the same kernels: a Llama-2-13B-like layer (d 5120, 40
+# heads, F 13824: 20 GEMM column tiles, 80 K-steps) and a grouped-query variant whose 5 KV
+# heads do not split evenly over the 8 XCDs (attention's plain head order).
+WIDE_CASES = [
+    dict(d_model=5120, n_heads=40, n_kv_heads=40, ffn_dim=13824),
+    dict(d_model=5120, n_heads=40, n_kv_heads=5, ffn_dim=13824),
+]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("shape", WIDE_CASES, ids=["13b-mha", "13b-gqa-5kv"])
+def test_bf16_wider_layer_shapes_vs_oracle(shape):
+    lengths = [1, 37, 129, 300]
+    case = W.make_case(2, 0, n_layers=1, lengths=lengths, random_gains=True, **shape)
+    print(f"[prefill] wide shape {shape} lengths {lengths}", flush=True)
+    gpu = gpu_prefill(case, pp.pp_pack(lengths, 512))
+    name = f"d{shape['d_model']} H{shape['n_heads']}/{shape['n_kv_heads']}"
+    ref = _oracle(case)
+    errs = _check_bar(name, gpu, ref, 1)
+    floor = _check_bar(name + " bf16-floor", _floor(case), ref, 1)
+    _gate(name, errs, floor)
+
+
 def _floor(case, prompts=None):
     r = _oracle(case, rnd=D.round_bf16, prompts=prompts)
     return r.hidden, r.k, r.v
