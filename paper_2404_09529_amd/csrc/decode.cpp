@@ -48,9 +48,10 @@ void projections(const pp_config* c, Proj (&p)[4]) {
     p[3] = {d, c->ffn_dim};                                       // down
 }
 
-// bf16 steps of up to 64 prompts (d <= 4096) take the skinny GEMM for every projection.
+// bf16 steps of up to 64 prompts take the skinny GEMM for every projection when the fused
+// residual norm takes the width (d <= 8192).
 bool use_skinny(const pp_config* c, int k) {
-    if (c->dtype != PP_BF16 || c->d_model > 4096) return false;   // d: the fused residual norm's limit
+    if (c->dtype != PP_BF16 || !ppk::residual_rmsnorm_ok(c->d_model)) return false;
     Proj p[4];
     projections(c, p);
     for (const Proj& q : p)

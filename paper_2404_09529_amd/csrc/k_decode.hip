@@ -507,37 +507,46 @@ void launch_rowpair(int nmb, int N, hipStream_t s, const bf16* A, int64_t lda, i
 }
 
 // Residual add of a split-K projection fused with the RMSNorm that follows it, one workgroup
-// of d / 4 threads per prompt row, 4 consecutive elements per thread: x[m] += sum over splits
-// of part[.][m] (split order; all S loads of a thread issued together), stored back; then
-// out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * g.  S = 0: no pending projection.
-template <typename TO>
+// of d / (4 E) threads per prompt row, 4 E consecutive elements per thread (E = 1 up to
+// d = 4096, 2 up to 8192): x[m] += sum over splits of part[.][m] (split order; the loads of 4
+// splits issued together), stored back; then out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * g.
+// S = 0: no pending projection.
+template <typename TO, int E>
 __global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ part,
                                                                 int S, int k, int d, const float* __restrict__ g,
                                                                 TO* __restrict__ out, float eps) {
     __shared__ float red[16];
-    const int m = blockIdx.x, c = 4 * threadIdx.x;
+    const int m = blockIdx.x, c = 4 * E * threadIdx.x;
     float* xr = x + int64_t(m) * d + c;
-    f32x4 v = *reinterpret_cast<const f32x4*>(xr);
+    f32x4 v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = *reinterpret_cast<const f32x4*>(xr + 4 * e);
     if (S > 0) {
         const float* p = part + int64_t(m) * d + c;
         const int64_t stride = int64_t(k) * d;
         int s = 0;
         for (; s + 4 <= S; s += 4) {
-            const f32x4 a0 = *reinterpret_cast<const f32x4*>(p + s * stride);
-            const f32x4 a1 = *reinterpret_cast<const f32x4*>(p + (s + 1) * stride);
-            const f32x4 a2 = *reinterpret_cast<const f32x4*>(p + (s + 2) * stride);
-            const f32x4 a3 = *reinterpret_cast<const f32x4*>(p + (s + 3) * stride);
-            v += a0;
-            v += a1;
-            v += a2;
-            v += a3;
+            f32x4 a[4][E];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int e = 0; e < E; ++e) a[u][e] = *reinterpret_cast<const f32x4*>(p + (s + u) * stride + 4 * e);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int e = 0; e < E; ++e) v[e] += a[u][e];
         }
-        for (; s < S; ++s) v += *reinterpret_cast<const f32x4*>(p + s * stride);
-        *reinterpret_cast<f32x4*>(xr) = v;
+        for (; s < S; ++s)
+#pragma unroll
+            for (int e = 0; e < E; ++e) v[e] += *reinterpret_cast<const f32x4*>(p + s * stride + 4 * e);
+#pragma unroll
+        for (int e = 0; e < E; ++e) *reinterpret_cast<f32x4*>(xr + 4 * e) = v[e];
     }
     float ss = 0.f;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) ss = fmaf(v[e], v[e], ss);
+    for (int e = 0; e < E; ++e)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ss = fmaf(v[e][i], v[e][i], ss);
     ss = wave_sum(ss);
     const int nw = blockDim.x / 64;
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
@@ -545,14 +554,17 @@ __global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restric
     float tot = 0.f;
     for (int i = 0; i < nw; ++i) tot += red[i];
     const float r = rsqrtf(tot / static_cast<float>(d) + eps);
-    const f32x4 gg = *reinterpret_cast<const f32x4*>(g + c);
-    if constexpr (sizeof(TO) == 2) {
-        bf16x4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(v[e] * r * gg[e]);
-        *reinterpret_cast<bf16x4*>(out + int64_t(m) * d + c) = o;
-    } else {
-        *reinterpret_cast<f32x4*>(out + int64_t(m) * d + c) = v * r * gg;
+    for (int e = 0; e < E; ++e) {
+        const f32x4 gg = *reinterpret_cast<const f32x4*>(g + c + 4 * e);
+        if constexpr (sizeof(TO) == 2) {
+            bf16x4 o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[i] = static_cast<bf16>(v[e][i] * r * gg[i]);
+            *reinterpret_cast<bf16x4*>(out + int64_t(m) * d + c + 4 * e) = o;
+        } else {
+            *reinterpret_cast<f32x4*>(out + int64_t(m) * d + c + 4 * e) = v[e] * r * gg;
+        }
     }
 }
 
@@ -667,12 +679,24 @@ bool skinny_ok(int k, int N, int K) { return k >= 1 && k <= 64 && N % SG_ROWS ==
 
 void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
                       float eps, hipStream_t s) {
-    const int threads = d / 4;   // d % 256 == 0 and d <= 4096: whole wavefronts, at most 1024 threads
-    if (dtype_out == PP_BF16)
-        residual_rmsnorm_kernel<bf16><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<bf16*>(out), eps);
-    else
-        residual_rmsnorm_kernel<float><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<float*>(out), eps);
+    // whole wavefronts, at most 1024 threads: d % 256 == 0 up to 4096 (4 elements per thread),
+    // d % 512 == 0 up to 8192 (8), as residual_rmsnorm_ok checks
+    if (d <= 4096) {
+        const int threads = d / 4;
+        if (dtype_out == PP_BF16)
+            residual_rmsnorm_kernel<bf16, 1><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<bf16*>(out), eps);
+        else
+            residual_rmsnorm_kernel<float, 1><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<float*>(out), eps);
+    } else {
+        const int threads = d / 8;
+        if (dtype_out == PP_BF16)
+            residual_rmsnorm_kernel<bf16, 2><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<bf16*>(out), eps);
+        else
+            residual_rmsnorm_kernel<float, 2><<<k, threads, 0, s>>>(x, part, S, k, d, g, static_cast<float*>(out), eps);
+    }
 }
+
+bool residual_rmsnorm_ok(int d) { return d > 0 && (d <= 4096 ? d % 256 == 0 : d <= 8192 && d % 512 == 0); }
 
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
                  const DecodeEpi& ep, hipStream_t s) {

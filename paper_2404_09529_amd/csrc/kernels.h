@@ -157,6 +157,8 @@ void decode_gemm_o(int k, const AttnChunks& ac, const void* W, int64_t ldw, int 
 // out[m] = RMSNorm(x[m]) * g in dtype_out (PP_BF16 or PP_F32); k rows of d <= 4096.
 void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
                       float eps, hipStream_t s);
+// Widths residual_rmsnorm takes: d % 256 == 0 up to 4096, d % 512 == 0 up to 8192.
+bool residual_rmsnorm_ok(int d);
 
 // bf16 C = A W^T for k <= 64 rows (A [k, lda], W [N, ldw]) with the epilogue `epi`:
 // kSwiGLU and kQkvRope in the GEMM kernel itself (N % 32 == 0); kResidual leaves float32

@@ -98,10 +98,17 @@ def test_fp32_generate_matches_oracle(lengths, n_new, n_layers):
 
 
 # ----------------------------------------------------------------------------- bf16, teacher-forced
+# a width past 4096 (the fused residual norm's 8-elements-per-thread form), 13B-like
+WIDE = {"d5120": dict(d_model=5120, n_heads=40, n_kv_heads=40, ffn_dim=13824)}
+
+
 def _bf16_case(model_name, lengths, n_layers, seed=0):
-    s = W.MODELS[model_name]
-    return W.make_case(6, seed, lengths=lengths, random_gains=True, n_layers=n_layers, d_model=s.d_model,
-                       n_heads=s.n_heads, n_kv_heads=s.n_kv_heads, ffn_dim=s.ffn_dim)
+    if model_name in WIDE:
+        dims = WIDE[model_name]
+    else:
+        s = W.MODELS[model_name]
+        dims = dict(d_model=s.d_model, n_heads=s.n_heads, n_kv_heads=s.n_kv_heads, ffn_dim=s.ffn_dim)
+    return W.make_case(6, seed, lengths=lengths, random_gains=True, n_layers=n_layers, **dims)
 
 
 @pytest.mark.parametrize("model_name,lengths,n_layers,n_new", [
@@ -112,6 +119,7 @@ def _bf16_case(model_name, lengths, n_layers, seed=0):
     ("mistral-7b", [4, 9, 1, 33] * 10, 1, 2),                        # 40 prompts: three blocks, GQA
     ("llama-1.3b", [2, 11, 6, 1] * 16, 1, 2),                        # 64 prompts: four blocks
     ("mistral-7b", [3, 8, 1, 20] * 16, 1, 2),                        # 64 prompts, d 4096: 96 KB staged slice
+    ("d5120", [37, 1, 300, 5], 1, 3),                                 # d 5120
 ])
 def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     case = _bf16_case(model_name, lengths, n_layers)
@@ -165,6 +173,7 @@ def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
 @pytest.mark.parametrize("model_name,lengths,n_layers", [
     ("llama-1.3b", [1, 300, 7, 129, 1, 64], 1),
     ("mistral-7b", [700, 2, 33], 1),
+    ("d5120", [2, 150, 9], 1),
 ])
 def test_packed_and_padded_generation_are_bit_identical(model_name, lengths, n_layers):
     case = _bf16_case(model_name, lengths, n_layers, seed=1)
