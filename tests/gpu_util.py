@@ -39,6 +39,19 @@ def rand_bf16(rng, shape, scale=1.0):
     return D.round_bf16(rng.standard_normal(shape).astype(np.float32) * np.float32(scale))
 
 
+def oracle_weights(w):
+    """The same weights as float64 arrays (exact: every value is a float32), so that the
+    oracle's float64 products do not convert them again on every call; its results are
+    unchanged."""
+    if isinstance(w, dict):
+        return {k: oracle_weights(v) for k, v in w.items()}
+    if isinstance(w, (list, tuple)):
+        return type(w)(oracle_weights(v) for v in w)
+    if isinstance(w, np.ndarray) and w.dtype == np.float32:
+        return w.astype(np.float64)
+    return w
+
+
 def bf16_ulp(x):
     """Spacing of bf16 numbers at |x| (8 significant bits)."""
     a = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), np.finfo(np.float32).tiny)

@@ -23,7 +23,7 @@ from oracle import generate as G
 from paper_2404_09529_amd import prepack as pp
 from paper_2404_09529_amd import workloads as W
 
-from .gpu_util import bf16_dev, f32_dev, gate_vs_floor, host64, i32_dev, report, require_gpu
+from .gpu_util import bf16_dev, f32_dev, gate_vs_floor, host64, i32_dev, oracle_weights, report, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -83,11 +83,12 @@ def test_fp32_generate_matches_oracle(lengths, n_new, n_layers):
     torch.cuda.synchronize()
     got = np.concatenate([first.cpu().numpy()[None], toks.cpu().numpy()]).T     # [k, 1 + n_new]
     picks = range(len(lengths)) if len(lengths) <= 8 else [0, 33, 69]
+    w64, lm64 = oracle_weights(case.weights), lm_head.astype(np.float64)
     for i in picks:
         p = _prompts(case)[i]
-        ref = G.generate(p, case.weights, sh, lm_head, n_new + 1)
-        f = G.teacher_forced(p, ref[:-1], case.weights, sh, lm_head)
-        gaps = [_gap(D.prefill_prompt(p, case.weights, sh).hidden[-1] @ lm_head.T)] + [_gap(r) for r in f.logits]
+        ref = G.generate(p, w64, sh, lm64, n_new + 1)
+        f = G.teacher_forced(p, ref[:-1], w64, sh, lm64)
+        gaps = [_gap(D.prefill_prompt(p, w64, sh).hidden[-1] @ lm64.T)] + [_gap(r) for r in f.logits]
         clear = next((t for t, g in enumerate(gaps) if g <= 1e-3), len(gaps))
         assert got[i][:clear].tolist() == ref[:clear].tolist(), (i, got[i].tolist(), ref.tolist())
         if clear == len(gaps):   # same tokens fed: the generated rows compare one to one
@@ -130,9 +131,10 @@ def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     model, pre, lm, _ = _prefill(case, lm_head)
     gen = pp.Generation(model, pre, case.lengths, n_new)
     prompts = _prompts(case)
-    fed = np.stack([G.generate(p, case.weights, sh, lm_head, n_new + 1) for p in prompts])   # oracle's greedy
-    ref = [G.teacher_forced(p, fed[i, :n_new], case.weights, sh, lm_head) for i, p in enumerate(prompts)]
-    flo = [G.teacher_forced(p, fed[i, :n_new], case.weights, sh, lm_head, rnd=D.round_bf16)
+    w64, lm64 = oracle_weights(case.weights), lm_head.astype(np.float64)
+    fed = np.stack([G.generate(p, w64, sh, lm64, n_new + 1) for p in prompts])   # oracle's greedy
+    ref = [G.teacher_forced(p, fed[i, :n_new], w64, sh, lm64) for i, p in enumerate(prompts)]
+    flo = [G.teacher_forced(p, fed[i, :n_new], w64, sh, lm64, rnd=D.round_bf16)
            for i, p in enumerate(prompts)]
     logits = torch.empty((k, V), dtype=torch.float32, device="cuda")
     out = torch.empty(k, dtype=torch.int32, device="cuda")

@@ -24,7 +24,7 @@ from oracle import decoder as D
 from paper_2404_09529_amd import prepack as pp
 from paper_2404_09529_amd import workloads as W
 
-from .gpu_util import gate_vs_floor, gpu_prefill, i32_dev, report, require_gpu
+from .gpu_util import gate_vs_floor, gpu_prefill, i32_dev, oracle_weights, report, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -38,7 +38,7 @@ def _gpu():
 
 def _oracle(case, rnd=None, prompts=None):
     kw = {} if rnd is None else {"rnd": rnd}
-    return D.prefill_per_prompt(case.lengths, case.tokens, case.weights, D.Shape.of(case.shape),
+    return D.prefill_per_prompt(case.lengths, case.tokens, oracle_weights(case.weights), D.Shape.of(case.shape),
                                 prompts=prompts, **kw)
 
 
@@ -272,8 +272,9 @@ def test_longest_prompt_end_to_end(wid, n_layers):
     torch.cuda.empty_cache()
     shape, toks = D.Shape.of(case.shape), case.tokens[a:a + n]
     print(f"[parity] {name}: oracle on {len(rows)} query rows", flush=True)
-    ref = D.prefill_prompt(toks, case.weights, shape, last_rows=rows)
-    flo = D.prefill_prompt(toks, case.weights, shape, rnd=D.round_bf16, last_rows=rows)
+    w64 = oracle_weights(case.weights)
+    ref = D.prefill_prompt(toks, w64, shape, last_rows=rows)
+    flo = D.prefill_prompt(toks, w64, shape, rnd=D.round_bf16, last_rows=rows)
     got = [report(f"{name} hidden", hid, ref.hidden)]
     fl = [report(f"{name} floor hidden", flo.hidden, ref.hidden)]
     for l in range(n_layers):

@@ -14,7 +14,7 @@ from oracle import decoder as D
 from paper_2404_09529_amd import prepack as pp
 from paper_2404_09529_amd import workloads as W
 
-from .gpu_util import gate_vs_floor, gpu_prefill, report, require_gpu
+from .gpu_util import gate_vs_floor, gpu_prefill, oracle_weights, report, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -54,8 +54,9 @@ def test_sweep_batch_vs_oracle(model, bs, batch, n_layers):
     off = np.concatenate([[0], np.cumsum(case.lengths)])
     rows = np.concatenate([np.arange(off[i], off[i + 1]) for i in picks])
     shape = D.Shape.of(case.shape)
-    ref = D.prefill_per_prompt(case.lengths, case.tokens, case.weights, shape, prompts=picks)
-    flo = D.prefill_per_prompt(case.lengths, case.tokens, case.weights, shape, prompts=picks, rnd=D.round_bf16)
+    w64 = oracle_weights(case.weights)
+    ref = D.prefill_per_prompt(case.lengths, case.tokens, w64, shape, prompts=picks)
+    flo = D.prefill_per_prompt(case.lengths, case.tokens, w64, shape, prompts=picks, rnd=D.round_bf16)
     name = f"sweep {model} bs{bs}"
     gate_vs_floor(name, _errs(name, gpu, ref, n_layers, rows),
                   _errs(name + " floor", (flo.hidden, flo.k, flo.v), ref, n_layers, rows))
