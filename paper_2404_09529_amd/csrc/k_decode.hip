@@ -389,6 +389,47 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
     }
 }
 
+// The rowpair epilogue for prompt m and the 4 rows c .. c + 3 of each of the workgroup's two
+// 16-row blocks: a = block 0's sums, b = block 1's.
+template <int EPI>
+__device__ __forceinline__ void rowpair_epilogue(int g, int m, int c, const f32x4& a, const f32x4& b,
+                                                 const ppk::DecodeEpi& ep) {
+    if (EPI == ppk::kSwiGLU) {       // features 16 g + c .. + 3: gate a, up b
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(a[e]) * b[e]);
+        *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + 16 * g + c) = o;
+    } else {                         // QKV: dims i .. i + 3 (a) and i + 64 .. (b) of head g / 4
+        const ppk::QkvOut& qo = ep.qkv;
+        const int head = g >> 2, i = 16 * (g & 3) + c;
+        const bool rotate = head < qo.H + qo.Hkv;
+        bf16x4 lo, hi;
+        if (rotate) {
+            const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float2 t = cs[e];
+                lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
+                hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                lo[e] = static_cast<bf16>(a[e]);
+                hi[e] = static_cast<bf16>(b[e]);
+            }
+        }
+        bf16* dst;
+        if (head < qo.H)
+            dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
+        else
+            dst = static_cast<bf16*>(rotate ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
+                  (head - qo.H - (rotate ? 0 : qo.Hkv)) * 128;
+        *reinterpret_cast<bf16x4*>(dst + i) = lo;
+        *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+    }
+}
+
 // Decode projections whose epilogue needs two blocks of 16 weight rows together, SwiGLU (the
 // 16 gate rows and the 16 up rows of 16 features) and QKV (16 rotate-half pairs c, c + 64 of
 // a head): one workgroup per such 32 rows, its 4 wavefronts each taking a quarter of K, the
@@ -457,41 +498,157 @@ __global__ __launch_bounds__(256) void rowpair_gemm_kernel(const bf16* __restric
             a += red[w2][0][mb][l];
             b += red[w2][1][mb][l];
         }
-        if (EPI == ppk::kSwiGLU) {       // features 16 g + c .. + 3: gate a, up b
-            bf16x4 o;
+        rowpair_epilogue<EPI>(g, m, c, a, b, ep);
+    }
+}
+
+// Buffer descriptor word 3 for raw (unstructured) 32-bit-offset loads on gfx9-family parts.
+constexpr int kRsrcWord3 = 0x00020000;
+// s_waitcnt immediate: vmcnt(n) and lgkmcnt(0), expcnt not waited for (gfx9 encoding).
+constexpr int wait_vm_lgkm0(int n) { return ((n >> 4) << 14) | (n & 15) | 0x0070; }
+typedef __attribute__((address_space(3))) void lds_void;
+
+// The rowpair projections for up to 16 prompts with K = 512 NSEG: the same 32 rows per workgroup
+// and epilogue, the weights streamed as whole 1 KB row segments.  Chunk (s, nb) = the 16 rows of
+// block nb x K columns 512 s .. + 511; each wavefront loads 4 of its rows (one 1 KB load each)
+// straight into an LDS ring of NW chunks, which from HBM runs markedly faster than the 64-byte
+// pieces of 16 rows that register loads in the MFMA layout request.  Wavefront w takes columns
+// 128 w .. + 127 of every chunk (4 K-steps); its quarter of the prompts' rows (4 fragments per
+// segment) goes into registers one segment ahead of its use.  The quarters' sums are added
+// through LDS in wavefront order, as in rowpair_gemm_kernel.
+constexpr int RS_COLS = 512;                    // K columns of a chunk
+constexpr int RS_CHUNK_B = 16 * RS_COLS * 2;    // 16 KB
+
+// LDS swizzle of a 1 KB chunk row: 16-byte chunk q of row r at q ^ f(r), f placing r's bits 0, 1,
+// 2 at bits 0, 2, 3 (within each 256-byte bank window): a fragment read (rows r..r+15, chunk
+// 16 w + 4 s + l / 16; lanes i and i + 32 served together) hits 16 distinct bank groups.
+__device__ __forceinline__ int rs_swz(int r) { return (r & 1) | (((r >> 1) & 1) << 2) | (((r >> 2) & 1) << 3); }
+
+template <int EPI, int NSEG, int NW>
+__global__ __launch_bounds__(256, 2) void rowpair_seg_kernel(const bf16* __restrict__ A, int64_t lda, int k,
+                                                             const bf16* __restrict__ W, int64_t ldw,
+                                                             ppk::DecodeEpi ep) {
+    static_assert(NW >= 2 && NW * RS_CHUNK_B >= 4 * 2 * 64 * 16, "ring, and room for the reduction");
+    constexpr int NCH = 2 * NSEG;               // chunks: segment-major, block nb within a segment
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lr = lane & 15, q4 = lane >> 4;
+    const int g = blockIdx.x;
+    int r0[2];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(a[e]) * b[e]);
-            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + 16 * g + c) = o;
-        } else {                         // QKV: dims i .. i + 3 (a) and i + 64 .. (b) of head g / 4
-            const ppk::QkvOut& qo = ep.qkv;
-            const int head = g >> 2, i = 16 * (g & 3) + c;
-            const bool rotate = head < qo.H + qo.Hkv;
-            bf16x4 lo, hi;
-            if (rotate) {
-                const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
+    for (int nb = 0; nb < 2; ++nb)
+        r0[nb] = EPI == ppk::kSwiGLU ? 32 * g + 16 * nb : (g >> 2) * 128 + 64 * nb + 16 * (g & 3);
+    // Consecutive workgroups are dispatched to consecutive XCDs, so the workgroups that share
+    // an XCD are g, g + 8, g + 16, ...; each starts its sweep over the K segments at segment
+    // (g / 8) mod NSEG.  Without the stagger all the workgroups of an XCD read the same 1 KB
+    // column segment at the same moment, and the kernel's time depended on which XCD received
+    // workgroup 0, which varies with the hardware queue that serves the stream: 31 to 43 us for
+    // the 7B gate/up projection, against 31 us on every queue with it.
+    const int rot = (g >> 3) & (NSEG - 1);
+    // one descriptor over rows r0[0] .. r0[1] + 15 (80 rows at most)
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>(W + int64_t(r0[0]) * ldw), 0, static_cast<int>((int64_t(r0[1] - r0[0] + 15) * ldw + RS_COLS * NSEG) * 2),
+        kRsrcWord3);
+    auto issue = [&](int c) {                   // chunk c (clamped) into slot c % NW
+        const int cc = c < NCH ? c : NCH - 1, sg = cc >> 1, nb = cc & 1;
+        char* slot = smem + (c % NW) * RS_CHUNK_B;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float2 t = cs[e];
-                    lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
-                    hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
-                }
-            } else {
+        for (int t = 0; t < 4; ++t) {
+            const int r = 4 * w + t;
+            const int soff =
+                static_cast<int>((int64_t(r0[nb] - r0[0] + r) * ldw + ((sg + rot) & (NSEG - 1)) * RS_COLS) * 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, (lds_void*)(slot + r * 1024), 16, 16 * (lane ^ rs_swz(r)),
+                                                     soff, 0, 0);
+        }
+    };
+    // the weight stream starts first; this wavefront's quarter of the prompt rows (rows past
+    // k read as row k - 1; never stored) follows one segment at a time: segment 0's now,
+    // segment sg + 1's at the first chunk of segment sg, so that its loads complete, in issue
+    // order, with the weight chunk the next segment starts on
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    lo[e] = static_cast<bf16>(a[e]);
-                    hi[e] = static_cast<bf16>(b[e]);
-                }
-            }
-            bf16* dst;
-            if (head < qo.H)
-                dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
-            else
-                dst = static_cast<bf16*>(rotate ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
-                      (head - qo.H - (rotate ? 0 : qo.Hkv)) * 128;
-            *reinterpret_cast<bf16x4*>(dst + i) = lo;
-            *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+    for (int c = 0; c < NW - 1; ++c) issue(c);
+    __builtin_amdgcn_sched_barrier(0);
+    const bf16* arow = A + int64_t(min(lr, k - 1)) * lda + 128 * w + 8 * q4;
+    bf16x8 pf[NSEG][4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) pf[0][st] = *reinterpret_cast<const bf16x8*>(arow + rot * RS_COLS + 32 * st);
+    f32x4 acc[2] = {};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        // chunk c is in when at most the loads of chunks c + 1 .. c + NW - 2 (4 each) are pending
+        // (later register loads only make the wait stricter)
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(4 * (NW - 2)));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue(c + NW - 1);                      // into the slot every wavefront finished at c - 1
+        const char* slot = smem + (c % NW) * RS_CHUNK_B;
+        const int sg = c >> 1, nb = c & 1;
+        if (nb == 0 && sg + 1 < NSEG) {
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+                pf[sg + 1][st] =
+                    *reinterpret_cast<const bf16x8*>(arow + ((sg + 1 + rot) & (NSEG - 1)) * RS_COLS + 32 * st);
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            const bf16x8 wf = *reinterpret_cast<const bf16x8*>(slot + lr * 1024 +
+                                                               16 * ((16 * w + 4 * st + q4) ^ rs_swz(lr)));
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, pf[sg][st], acc[nb], 0, 0, 0);
         }
     }
+    // the clamped loads past the last chunk land before the ring's LDS is reused
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+    __syncthreads();
+    f32x4* red = reinterpret_cast<f32x4*>(smem);   // [w][nb][lane]
+    red[(w * 2 + 0) * 64 + lane] = acc[0];
+    red[(w * 2 + 1) * 64 + lane] = acc[1];
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const int l = threadIdx.x, m = l & 15, c = 4 * (l >> 4);
+        if (m < k) {
+            f32x4 a = red[l], b = red[64 + l];
+#pragma unroll
+            for (int w2 = 1; w2 < 4; ++w2) {
+                a += red[(w2 * 2) * 64 + l];
+                b += red[(w2 * 2 + 1) * 64 + l];
+            }
+            rowpair_epilogue<EPI>(g, m, c, a, b, ep);
+        }
+    }
+}
+
+template <int EPI, int NSEG, int NW>
+void launch_rowpair_seg(int N, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W, int64_t ldw,
+                        const ppk::DecodeEpi& ep) {
+    constexpr int lds = NW * RS_CHUNK_B;
+    static bool attr = [] {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&rowpair_seg_kernel<EPI, NSEG, NW>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        return true;
+    }();
+    (void)attr;
+    rowpair_seg_kernel<EPI, NSEG, NW><<<N / 32, 256, lds, s>>>(A, lda, k, W, ldw, ep);
+}
+
+// Whether rowpair_seg_kernel takes the shape: up to 16 prompts, K = 2048 or 4096.  The ring
+// depth follows the grid: three workgroups of 48 KB per CU when there are more than 512 of
+// them, else two of 64 KB.
+template <int EPI>
+bool launch_rowpair_seg_for(int N, int K, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W,
+                            int64_t ldw, const ppk::DecodeEpi& ep) {
+    if (k > 16 || (K != 2048 && K != 4096)) return false;
+    const bool wide = N / 32 > 512;
+    if (K == 4096) {
+        if (wide) launch_rowpair_seg<EPI, 8, 3>(N, s, A, lda, k, W, ldw, ep);
+        else launch_rowpair_seg<EPI, 8, 4>(N, s, A, lda, k, W, ldw, ep);
+    } else {
+        if (wide) launch_rowpair_seg<EPI, 4, 3>(N, s, A, lda, k, W, ldw, ep);
+        else launch_rowpair_seg<EPI, 4, 4>(N, s, A, lda, k, W, ldw, ep);
+    }
+    return true;
 }
 
 template <int EPI>
@@ -703,8 +860,16 @@ void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int6
     const int nmb = (k + 15) / 16;
     const bf16* a = static_cast<const bf16*>(A);
     const bf16* w = static_cast<const bf16*>(W);
-    if (epi == kSwiGLU) return launch_rowpair<kSwiGLU>(nmb, N, s, a, lda, k, w, ldw, K, ep);
-    if (epi == kQkvRope) return launch_rowpair<kQkvRope>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+    if (epi == kSwiGLU) {
+        if (!launch_rowpair_seg_for<kSwiGLU>(N, K, s, a, lda, k, w, ldw, ep))
+            launch_rowpair<kSwiGLU>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+        return;
+    }
+    if (epi == kQkvRope) {
+        if (!launch_rowpair_seg_for<kQkvRope>(N, K, s, a, lda, k, w, ldw, ep))
+            launch_rowpair<kQkvRope>(nmb, N, s, a, lda, k, w, ldw, K, ep);
+        return;
+    }
     // kResidual: split-K partial sums, added to the residual stream by residual_rmsnorm
     const SkinnySplit sp = skinny_split(N, K);
     const AttnChunks none{};
