@@ -88,8 +88,9 @@ Layout layout_of(const pp_config* c, const pp_gen_dlayout* g) {
     if (use_skinny(c, g->k)) {
         Proj p[4];
         projections(c, p);
-        for (int i : {1, 3})   // O and down leave split-K partial sums
-            gpart = std::max(gpart, size_t(ppk::skinny_split(p[i].N, p[i].K).splits) * k * p[i].N * 4);
+        // O and down leave split-K partial sums
+        gpart = std::max(size_t(ppk::skinny_split(p[1].N, p[1].K).splits) * k * p[1].N * 4,
+                         size_t(ppk::decode_gemm_splits(g->k, p[3].N, p[3].K)) * k * p[3].N * 4);
     }
     L.gpart = take(gpart);
     L.total = off;
@@ -214,7 +215,7 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
                              ppk::DecodeEpi{act, F, none}, s);
             ppk::decode_gemm(ppk::kResidual, act, F, k, w->w_down[l], F, d, F, gpart,
                              ppk::DecodeEpi{x, d, none}, s);
-            pending = ppk::skinny_split(d, F).splits;
+            pending = ppk::decode_gemm_splits(k, d, F);
         } else if (bf) {
             ppk::gemm_bf16(ppk::kSwiGLU, xn, d, w->w_gateup[l], d, act, F, k, 2 * F, d, nullptr, 0, s);
             ppk::gemm_bf16(ppk::kResidual, act, F, w->w_down[l], F, x, d, k, d, F, nullptr, 0, s);

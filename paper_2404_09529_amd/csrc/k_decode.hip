@@ -22,13 +22,17 @@
 //                        features), K split four ways across its wavefronts and added
 //                        through LDS; RoPE with the query store and the key/value append,
 //                        or SwiGLU, in the same kernel.
-// skinny_gemm_kernel     O and down (N = d, too few rows for one workgroup per 32): about
-//                        512 pieces of 64 rows x a K split of up to 6 tiles of 128; each
-//                        workgroup stages its slice of A (k rows, LDS sized to k) once and
-//                        each wavefront streams 16 weight rows into the 16x16x32 bf16 MFMA,
-//                        all its K steps requested up front; float32 partial sums per
-//                        split.  For O the staged slice is the attention output, merged
-//                        there from the chunk results.
+// rowpair_seg_kernel     the same for up to 16 prompts at K = 2048 or 4096, the weights
+//                        loaded as whole 1 KB row segments straight into an LDS ring.
+// splitk_seg_kernel      down (N = d) for up to 16 prompts in that style: 32 rows x a K
+//                        split per workgroup, float32 partial sums per split.
+// skinny_gemm_kernel     O, and down for more prompts (N = d, too few rows for one
+//                        workgroup per 32): about 512 pieces of 64 rows x a K split of up to
+//                        6 tiles of 128; each workgroup stages its slice of A (k rows, LDS
+//                        sized to k) once and each wavefront streams 16 weight rows into the
+//                        16x16x32 bf16 MFMA, all its K steps requested up front; float32
+//                        partial sums per split.  For O the staged slice is the attention
+//                        output, merged there from the chunk results.
 // residual_rmsnorm_kernel  adds those partial sums, in split order, to the residual stream
 //                        inside the RMSNorm that follows each projection.
 // (A single-kernel split-K with the sum done by the last workgroup of a row group was
@@ -651,6 +655,147 @@ bool launch_rowpair_seg_for(int N, int K, hipStream_t s, const bf16* A, int64_t 
     return true;
 }
 
+// Split-K projection for up to 16 prompts (the down projection, whose N = d leaves too few
+// 32-row groups for one workgroup each), the weights streamed as 1 KB row segments as in
+// rowpair_seg_kernel: workgroup (g, s) takes rows 32 g .. + 31 and split s of the K / 512
+// segments (splits differ by at most one segment, none holds more than S), two 16-row blocks
+// per segment through an LDS ring of NW chunks, and leaves float32 partial sums
+// part[s][m][n] for residual_rmsnorm to add in split order.  When K ends in part of a segment
+// (K % 512 = 128, 256 or 384), the 16-byte pieces past K of that segment's rows read pieces
+// inside it instead and the prompt columns past K are zeros, so those weights add exact
+// zeros.  Chunks past a short split's segments re-read its first one (in bounds, never
+// used), which keeps 4 loads per chunk step for the fixed wait counts.
+template <int S, int NW>
+__global__ __launch_bounds__(256, 2) void splitk_seg_kernel(const bf16* __restrict__ A, int64_t lda, int k,
+                                                            const bf16* __restrict__ W, int64_t ldw, int N, int K,
+                                                            float* __restrict__ part) {
+    static_assert(NW >= 2 && NW * RS_CHUNK_B >= 4 * 2 * 64 * 16, "ring, and room for the reduction");
+    constexpr int NCH = 2 * S;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lr = lane & 15, q4 = lane >> 4;
+    const int g = blockIdx.x, sp = blockIdx.y, splits = gridDim.y;
+    const int nseg = (K + RS_COLS - 1) / RS_COLS;
+    const int tail = K - (nseg - 1) * RS_COLS;   // columns of the last segment: 128 .. 512
+    const int s_lo = sp * nseg / splits, n_here = (sp + 1) * nseg / splits - s_lo;   // 1 .. S
+    // the workgroups that share an XCD (consecutive linear ids go to consecutive XCDs) start
+    // their sweeps at different segments of the split
+    const int rot = ((g + gridDim.x * sp) >> 3) % n_here;
+    const int r0 = 32 * g;
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>(W + int64_t(r0) * ldw), 0, static_cast<int>((31 * ldw + K) * 2), kRsrcWord3);
+    auto seg_of = [&](int sl) {               // the segment the split's sl-th chunk pair reads
+        if (sl >= n_here) return s_lo;
+        const int p = sl + rot;
+        return s_lo + (p >= n_here ? p - n_here : p);
+    };
+    auto issue = [&](int c) {                 // chunk c (clamped) into slot c % NW
+        const int cc = c < NCH ? c : NCH - 1, sl = cc >> 1, nb = cc & 1;
+        const int sg = seg_of(sl);
+        const int qv = sg == nseg - 1 ? tail / 8 : 64;   // 16-byte pieces inside K
+        char* slot = smem + (c % NW) * RS_CHUNK_B;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int r = 4 * w + t;
+            const int soff = static_cast<int>((int64_t(16 * nb + r) * ldw + int64_t(sg) * RS_COLS) * 2);
+            const int q = lane ^ rs_swz(r);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, (lds_void*)(slot + r * 1024), 16, 16 * (q < qv ? q : q & 15),
+                                                     soff, 0, 0);
+        }
+    };
+    // this wavefront's quarter of the prompt rows for the split's sl-th segment (rows past k
+    // read as row k - 1, never stored; columns past K as zeros)
+    const bf16* arow = A + int64_t(min(lr, k - 1)) * lda + 128 * w + 8 * q4;
+    auto prompt = [&](int sl, bf16x8* f) {
+        const int sg = seg_of(sl);
+        const bool past = sl >= n_here || (sg == nseg - 1 && 128 * w >= tail);
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+            f[st] = past ? bf16x8{} : *reinterpret_cast<const bf16x8*>(arow + int64_t(sg) * RS_COLS + 32 * st);
+    };
+#pragma unroll
+    for (int c = 0; c < NW - 1; ++c) issue(c);
+    __builtin_amdgcn_sched_barrier(0);
+    bf16x8 pf[S][4];
+    prompt(0, pf[0]);
+    f32x4 acc[2] = {};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        // chunk c is in when at most the loads of chunks c + 1 .. c + NW - 2 (4 each) are pending
+        // (later register loads only make the wait stricter)
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(4 * (NW - 2)));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue(c + NW - 1);                    // into the slot every wavefront finished at c - 1
+        const char* slot = smem + (c % NW) * RS_CHUNK_B;
+        const int sl = c >> 1, nb = c & 1;
+        if (nb == 0 && sl + 1 < S) prompt(sl + 1, pf[sl + 1]);
+        if (sl < n_here) {
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const bf16x8 wf = *reinterpret_cast<const bf16x8*>(slot + lr * 1024 +
+                                                                   16 * ((16 * w + 4 * st + q4) ^ rs_swz(lr)));
+                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, pf[sl][st], acc[nb], 0, 0, 0);
+            }
+        }
+    }
+    // the clamped loads past the last chunk land before the ring's LDS is reused
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+    __syncthreads();
+    f32x4* red = reinterpret_cast<f32x4*>(smem);   // [w][nb][lane]
+    red[(w * 2 + 0) * 64 + lane] = acc[0];
+    red[(w * 2 + 1) * 64 + lane] = acc[1];
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const int l = threadIdx.x, m = l & 15, c = 4 * (l >> 4);
+        if (m < k) {
+            f32x4 a = red[l], b = red[64 + l];
+#pragma unroll
+            for (int w2 = 1; w2 < 4; ++w2) {
+                a += red[(w2 * 2) * 64 + l];
+                b += red[(w2 * 2 + 1) * 64 + l];
+            }
+            float* dst = part + (int64_t(sp) * k + m) * N + r0 + c;
+            *reinterpret_cast<f32x4*>(dst) = a;
+            *reinterpret_cast<f32x4*>(dst + 16) = b;
+        }
+    }
+}
+
+template <int S, int NW>
+void launch_splitk_seg(int N, int splits, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W,
+                       int64_t ldw, int K, float* part) {
+    constexpr int lds = NW * RS_CHUNK_B;
+    static bool attr = [] {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&splitk_seg_kernel<S, NW>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        return true;
+    }();
+    (void)attr;
+    splitk_seg_kernel<S, NW><<<dim3(N / 32, splits), 256, lds, s>>>(A, lda, k, W, ldw, N, K, part);
+}
+
+// splitk_seg_kernel's split: the most segments per split (4, 2 or 1) that still gives at least
+// 256 workgroups (at the 7B shape 4 segments, 768 workgroups, three per CU; at 1.3B 2, 384:
+// 1 segment per workgroup and 8 per split were slower there, as were 4-chunk rings); s = 0
+// when the kernel does not take the shape (more than 16 prompts, N % 32 or K % 128 not zero).
+struct SegSplit {
+    int s, splits;
+};
+SegSplit seg_split(int k, int N, int K) {
+    if (k < 1 || k > 16 || N % 32 != 0 || K % 128 != 0 || K <= 0) return SegSplit{0, 0};
+    const int nseg = (K + RS_COLS - 1) / RS_COLS, groups = N / 32;
+    int s = 4, splits = (nseg + 3) / 4;
+    while (s > 1 && groups * splits < 256) {
+        s /= 2;
+        splits = (nseg + s - 1) / s;
+    }
+    return SegSplit{s, splits};
+}
+
 template <int EPI>
 void launch_rowpair(int nmb, int N, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W, int64_t ldw,
                     int K, const ppk::DecodeEpi& ep) {
@@ -832,6 +977,11 @@ SkinnySplit skinny_split(int N, int K) {
     return SkinnySplit{per, (tiles + per - 1) / per};
 }
 
+int decode_gemm_splits(int k, int N, int K) {
+    const SegSplit ss = seg_split(k, N, K);
+    return ss.s ? ss.splits : skinny_split(N, K).splits;
+}
+
 bool skinny_ok(int k, int N, int K) { return k >= 1 && k <= 64 && N % SG_ROWS == 0 && K % SG_TILE == 0; }
 
 void residual_rmsnorm(int dtype_out, float* x, const float* part, int S, int k, int d, const float* g, void* out,
@@ -871,6 +1021,13 @@ void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int6
         return;
     }
     // kResidual: split-K partial sums, added to the residual stream by residual_rmsnorm
+    const SegSplit ss = seg_split(k, N, K);
+    switch (ss.s) {
+        case 4: return launch_splitk_seg<4, 3>(N, ss.splits, s, a, lda, k, w, ldw, K, part);
+        case 2: return launch_splitk_seg<2, 3>(N, ss.splits, s, a, lda, k, w, ldw, K, part);
+        case 1: return launch_splitk_seg<1, 3>(N, ss.splits, s, a, lda, k, w, ldw, K, part);
+        default: break;   // s = 0: the skinny kernel
+    }
     const SkinnySplit sp = skinny_split(N, K);
     const AttnChunks none{};
     launch_skinny<false>(sp.tiles_per_split, nmb, dim3(N / SG_ROWS, sp.splits), s, a, lda, k, w, ldw, N, K, part,

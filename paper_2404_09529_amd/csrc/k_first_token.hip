@@ -305,6 +305,10 @@ __global__ __launch_bounds__(256, 1) void lm_head_seg_kernel(const bf16* __restr
     const int nb0 = blockIdx.x * LM_ROWS;
     const int lr = lane & 15, q4 = lane >> 4;
     const int n_seg = d / SEG_COLS;
+    // workgroups on one XCD (blockIdx.x, + 8, + 16, ...) start their sweep over the K segments
+    // at different segments, so that they do not all read the same 1 KB column of their rows
+    // at the same moment (from HBM: 59.4 -> 56.5 us for 64 prompts at vocabulary 32000)
+    const int rot = (blockIdx.x >> 3) % n_seg;
     const int rows_p = k_pad;                                  // prompt rows present (<= 64)
     const int last_row = min(V - 1 - nb0, LM_ROWS - 1);
     const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
@@ -315,7 +319,9 @@ __global__ __launch_bounds__(256, 1) void lm_head_seg_kernel(const bf16* __restr
     // l ^ f(r) (lm_swz<128>: within each 256-byte bank window, so fragment reads of 8 rows x
     // chunks {c, c ^ 2} hit 16 distinct bank groups)
     auto w_issue = [&](int g) {       // chunk g (clamped: dead chunks re-read the last) -> slot g % NW
-        const int gc = min(g, 8 * n_seg - 1), sg = gc >> 3, rb = gc & 7;
+        const int gc = min(g, 8 * n_seg - 1), rb = gc & 7;
+        int sg = (gc >> 3) + rot;
+        if (sg >= n_seg) sg -= n_seg;
         char* slot = smem + (g % NW) * SEG_W_B;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -326,7 +332,8 @@ __global__ __launch_bounds__(256, 1) void lm_head_seg_kernel(const bf16* __restr
         }
     };
     auto p_issue = [&](int sg, int i) {   // quarter i of the prompt tile of segment sg (clamped)
-        const int sc = min(sg, n_seg - 1);
+        int sc = min(sg, n_seg - 1) + rot;
+        if (sc >= n_seg) sc -= n_seg;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int r = 16 * wave + 4 * i + t;

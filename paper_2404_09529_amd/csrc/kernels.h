@@ -162,8 +162,11 @@ bool residual_rmsnorm_ok(int d);
 
 // bf16 C = A W^T for k <= 64 rows (A [k, lda], W [N, ldw]) with the epilogue `epi`:
 // kSwiGLU and kQkvRope in the GEMM kernel itself (N % 32 == 0); kResidual leaves float32
-// partial sums in part (splits * k * N floats) for residual_rmsnorm to add.
+// partial sums in part (decode_gemm_splits(k, N, K) * k * N floats) for residual_rmsnorm to
+// add.
 void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int64_t ldw, int N, int K, float* part,
                  const DecodeEpi& ep, hipStream_t s);
+// The number of K splits decode_gemm's kResidual leaves for k rows of an N x K product.
+int decode_gemm_splits(int k, int N, int K);
 
 }  // namespace ppk

@@ -121,6 +121,7 @@ def _bf16_case(model_name, lengths, n_layers, seed=0):
     ("llama-1.3b", [2, 11, 6, 1] * 16, 1, 2),                        # 64 prompts: four blocks
     ("mistral-7b", [3, 8, 1, 20] * 16, 1, 2),                        # 64 prompts, d 4096: 96 KB staged slice
     ("d5120", [37, 1, 300, 5], 1, 3),                                 # d 5120
+    ("llama2-7b", [37, 1, 300, 5], 1, 3),                             # F 11008: down ends in half a 1 KB segment
 ])
 def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     case = _bf16_case(model_name, lengths, n_layers)
@@ -176,6 +177,7 @@ def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     ("llama-1.3b", [1, 300, 7, 129, 1, 64], 1),
     ("mistral-7b", [700, 2, 33], 1),
     ("d5120", [2, 150, 9], 1),
+    ("llama2-7b", [2, 150, 9, 1], 1),
 ])
 def test_packed_and_padded_generation_are_bit_identical(model_name, lengths, n_layers):
     case = _bf16_case(model_name, lengths, n_layers, seed=1)
