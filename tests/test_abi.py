@@ -370,15 +370,23 @@ def test_decode_workspace_and_rejections(L):
     assert L.pp_decode_workspace_size(ctypes.byref(cfg), ctypes.byref(gl), ctypes.byref(n)) == pp.PP_OK
     k, d, H, D, F = 3, 4096, 32, 128, 14336
     chunks = 3 + 1                                          # ceil(300 / 128) context + 1 generated
-    # split-K partial sums of the O and down projections (one row per prompt): about 512
-    # workgroups of 64 rows x up to 6 tiles of 128 columns; the larger one sets the size
+    # split-K partial sums of the O and down projections (one row per prompt); the larger one
+    # sets the size.  O: about 512 workgroups of 64 rows x up to 6 tiles of 128 columns.
     def splits(N, K):
         tiles, groups = K // 128, N // 64
         target = max(1, -(-512 // groups))
         per = min(6, max(1, -(-tiles // target)))
         return -(-tiles // per)
+    # down, up to 16 prompts: the K / 512 segments in splits of at most 4, 2 or 1 (the most
+    # that still gives 256 workgroups of 32 rows), near-equal in size
+    def seg_splits(N, K):
+        nseg, groups = -(-K // 512), N // 32
+        for s in (4, 2):
+            if groups * -(-nseg // s) >= 256:
+                return -(-nseg // s)
+        return nseg
     proj = [(48 * 128, d), (d, H * D), (2 * F, d), (d, F)]
-    gpart = max(splits(N, K) * k * N * 4 for N, K in (proj[1], proj[3]))   # O and down
+    gpart = max(splits(*proj[1]) * k * proj[1][0] * 4, seg_splits(*proj[3]) * k * proj[3][0] * 4)
     want = (k * d * 4 + k * d * 2 + k * H * D * 2 + k * H * D * 2 + k * F * 2 + k * d * 4
             + k * H * chunks * (D + 4) * 4 + k * 64 * 8 + (4 * k + 1) * 4 + 16 * d * 2 + 250 * k * 8
             + gpart)
