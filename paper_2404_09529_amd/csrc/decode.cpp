@@ -162,8 +162,12 @@ void enqueue_step(const pp_config* cfg, const pp_weights* w, const pp_gen_dlayou
     int32_t* slot_seg = slot_kv + k;
     int32_t* ident = slot_seg + k;        // k + 1 entries
     const size_t ctx_layer = size_t(g->ctx_rows) * kvw * e, gen_layer = size_t(g->gen_rows) * kvw * e;
-    const ppk::DecodeLayout Ly{k, chunks(g->max_len), chunks(g->n_new), g->ctx_off, g->ctx_span, g->ctx_valid,
-                               g->pos0, g->gen_off};
+    // the prompts' context chunks together: at most ceil(ctx_rows / chunk) + k, as every prompt's
+    // span lies in its own ctx_rows (and at most k x the longest prompt's)
+    const int n_ctx_items = static_cast<int>(std::min<int64_t>(int64_t(k) * chunks(g->max_len),
+                                                               (g->ctx_rows + ppk::kDecodeChunk - 1) / ppk::kDecodeChunk + k));
+    const ppk::DecodeLayout Ly{k, chunks(g->max_len), chunks(g->n_new), n_ctx_items, g->ctx_off, g->ctx_span,
+                               g->ctx_valid, g->pos0, g->gen_off};
     const bool skinny = use_skinny(cfg, k);
     float* gpart = reinterpret_cast<float*>(ws + L.gpart);
 

@@ -116,21 +116,19 @@ __device__ __forceinline__ void merge(float& m, float& l, float* o, float m2, fl
     m = M;
 }
 
-// Lane l of wavefront w: key group kg = l / 8 (one key per iteration), dimension slice
-// dl = l % 8 (D / 8 consecutive elements).  Keys of the chunk: j0 + 8 IT w + 8 it + kg.
+// One (prompt i, key/value head g, chunk c) of the decode attention: the chunk's (max, sum,
+// output) for the group's R query heads into part.
 template <typename T, int D, int R>
-__global__ __launch_bounds__(256) void decode_attn_kernel(
+__device__ __forceinline__ void decode_attn_chunk(
     const T* __restrict__ q, int64_t ldq, const T* __restrict__ ctx_k, const T* __restrict__ ctx_v,
     const T* __restrict__ gen_k, const T* __restrict__ gen_v, int64_t ldkv, const int32_t* __restrict__ ctx_off,
     const int32_t* __restrict__ ctx_span, const int32_t* __restrict__ ctx_valid, const int32_t* __restrict__ gen_off,
-    int step, int Hkv, int n_ctx_chunks, int n_chunks, float* __restrict__ part) {
+    int step, int Hkv, int n_ctx_chunks, int n_chunks, float* __restrict__ part, int i, int g, int c) {
     constexpr int DL = D / 8;
     constexpr int PS = D + 4;            // floats per partial: o[D], m, l, 2 unused
     __shared__ float red[4][R][D + 2];
-    const int i = blockIdx.x / Hkv, g = blockIdx.x % Hkv, c = blockIdx.y;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int kg = lane >> 3, dl = lane & 7;
-
     const T* K;
     const T* V;
     int64_t row0;
@@ -150,7 +148,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
         K = gen_k;
         V = gen_v;
     }
-    if (j0 >= jend) return;              // past this prompt's keys: no partial, never combined
+    if (j0 >= jend) return;              // generated keys not there yet: no partial, never combined
 
     // queries of the group's R heads, pre-scaled so that scores are in base 2
     const float scale = kLog2e * rsqrtf(static_cast<float>(D));
@@ -250,6 +248,70 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(
             pp[D] = mm;
             pp[D + 1] = ll;
         }
+    }
+    __syncthreads();   // red is reused by the workgroup's next item
+}
+
+// The decode attention's work list: first the generated keys' chunks of every prompt
+// (k x n_gen_chunks, prompt-major), then each prompt's context chunks, prompt by prompt
+// (ceil(ctx_span / CH) each).  Item -> (prompt, chunk index into the partial results); an
+// item past the last context chunk -> prompt -1.  The context chunk counts are summed across
+// the lanes, 64 prompts at a time (every lane of the wavefront returns the same answer).
+__device__ __forceinline__ int2 attn_item(int item, int k, int n_gen_chunks, int n_ctx_chunks,
+                                          const int32_t* __restrict__ ctx_span) {
+    if (item < k * n_gen_chunks) return make_int2(item / n_gen_chunks, n_ctx_chunks + item % n_gen_chunks);
+    const int idx = item - k * n_gen_chunks;
+    const int lane = threadIdx.x & 63;
+    int base = 0;
+    for (int b = 0; b < k; b += 64) {
+        const int l = b + lane;
+        int p = l < k ? (ctx_span[l] + CH - 1) / CH : 0;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int t = __shfl_up(p, o);
+            if (lane >= o) p += t;
+        }
+        const int total = __shfl(p, 63);
+        if (idx < base + total) {
+            const int li = __popcll(__ballot(p + base <= idx));   // prompts of this block wholly before
+            const int before = li > 0 ? __shfl(p, li - 1) : 0;
+            return make_int2(b + li, idx - base - before);
+        }
+        base += total;
+    }
+    return make_int2(-1, 0);
+}
+
+// Lane l of wavefront w: key group kg = l / 8 (one key per iteration), dimension slice
+// dl = l % 8 (D / 8 consecutive elements).  Keys of the chunk: j0 + 8 IT w + 8 it + kg.
+// list == 0: workgroup (i Hkv + g, c) takes chunk c of prompt i and key/value head g, every
+// prompt n_ctx_chunks + n_gen_chunks of them (those past its keys return at once).
+// list != 0: workgroup (g, y) takes the work-list items y, y + gridDim.y, ... of head g (one
+// each when the grid holds them all), so only real chunks occupy the CUs: a batch of nine
+// 1-token prompts and one of 1000 at the 7B shape, 10.4 -> 9.6 us.  The host takes the list
+// when it is shorter; in the full-batching layout it is not, and the lookup would cost each
+// workgroup a dependent load (1.3B: 2% of the step).  bf16 with one query head per key/value
+// head: four workgroups per CU (at most 128 registers), as the chunks are latency-bound (at
+// 129 registers, three per CU, the 7B batch above took 11.6 us); the other forms would spill.
+template <typename T, int D, int R>
+__global__ __launch_bounds__(256, (R == 1 && sizeof(T) == 2) ? 4 : 1) void decode_attn_kernel(
+    const T* __restrict__ q, int64_t ldq, const T* __restrict__ ctx_k, const T* __restrict__ ctx_v,
+    const T* __restrict__ gen_k, const T* __restrict__ gen_v, int64_t ldkv, const int32_t* __restrict__ ctx_off,
+    const int32_t* __restrict__ ctx_span, const int32_t* __restrict__ ctx_valid, const int32_t* __restrict__ gen_off,
+    int step, int k, int Hkv, int n_ctx_chunks, int n_gen_chunks, int list, float* __restrict__ part) {
+    const int n_chunks = n_ctx_chunks + n_gen_chunks;
+    if (!list) {
+        decode_attn_chunk<T, D, R>(q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, ctx_off, ctx_span, ctx_valid, gen_off,
+                                   step, Hkv, n_ctx_chunks, n_chunks, part, blockIdx.x / Hkv, blockIdx.x % Hkv,
+                                   blockIdx.y);
+        return;
+    }
+    for (int item = blockIdx.y;; item += gridDim.y) {
+        const int2 ic = attn_item(item, k, n_gen_chunks, n_ctx_chunks, ctx_span);
+        const int i = __builtin_amdgcn_readfirstlane(ic.x), c = __builtin_amdgcn_readfirstlane(ic.y);
+        if (i < 0) return;
+        decode_attn_chunk<T, D, R>(q, ldq, ctx_k, ctx_v, gen_k, gen_v, ldkv, ctx_off, ctx_span, ctx_valid, gen_off,
+                                   step, Hkv, n_ctx_chunks, n_chunks, part, i, blockIdx.x, c);
     }
 }
 
@@ -912,11 +974,16 @@ template <typename T, int D, int R>
 void launch_attn(const void* q, int64_t ldq, const void* ctx_k, const void* ctx_v, const void* gen_k,
                  const void* gen_v, int64_t ldkv, const ppk::DecodeLayout& Ly, int step, int Hkv, float* part,
                  hipStream_t s) {
-    const dim3 grid(Ly.k * Hkv, Ly.n_ctx_chunks + Ly.n_gen_chunks);
+    // the work list when it is shorter than every prompt's n_ctx_chunks: one workgroup per item
+    // and key/value head (the kernel loops over any items past the grid's 65535 rows)
+    const bool list = Ly.n_ctx_items < int64_t(Ly.k) * Ly.n_ctx_chunks;
+    const int64_t items = int64_t(Ly.k) * Ly.n_gen_chunks + Ly.n_ctx_items;
+    const dim3 grid = list ? dim3(Hkv, static_cast<unsigned>(std::min<int64_t>(items, 65535)))
+                           : dim3(Ly.k * Hkv, Ly.n_ctx_chunks + Ly.n_gen_chunks);
     decode_attn_kernel<T, D, R><<<grid, 256, 0, s>>>(
         static_cast<const T*>(q), ldq, static_cast<const T*>(ctx_k), static_cast<const T*>(ctx_v),
         static_cast<const T*>(gen_k), static_cast<const T*>(gen_v), ldkv, Ly.ctx_off, Ly.ctx_span, Ly.ctx_valid,
-        Ly.gen_off, step, Hkv, Ly.n_ctx_chunks, Ly.n_ctx_chunks + Ly.n_gen_chunks, part);
+        Ly.gen_off, step, Ly.k, Hkv, Ly.n_ctx_chunks, Ly.n_gen_chunks, list ? 1 : 0, part);
 }
 
 template <typename T, int D>

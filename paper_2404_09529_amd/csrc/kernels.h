@@ -100,9 +100,11 @@ hipError_t first_token_scratch(void** ptr);
 constexpr int kDecodeChunk = 128;   // keys per workgroup of the decode attention
 
 // Device view of a generation layout (pp_gen_dlayout) with the chunk counts of its keys:
-// n_ctx_chunks = ceil(max_len / kDecodeChunk), n_gen_chunks = ceil(n_new / kDecodeChunk).
+// n_ctx_chunks = ceil(max_len / kDecodeChunk), n_gen_chunks = ceil(n_new / kDecodeChunk), and
+// n_ctx_items >= the context chunks of all prompts together (the decode attention's grid;
+// any it leaves out are taken by a second pass of its workgroups).
 struct DecodeLayout {
-    int k, n_ctx_chunks, n_gen_chunks;
+    int k, n_ctx_chunks, n_gen_chunks, n_ctx_items;
     const int32_t *ctx_off, *ctx_span, *ctx_valid, *pos0, *gen_off;
 };
 
