@@ -24,6 +24,8 @@
 //                        or SwiGLU, in the same kernel.
 // rowpair_seg_kernel     the same for up to 16 prompts at K = 2048 or 4096, the weights
 //                        loaded as whole 1 KB row segments straight into an LDS ring.
+// qkv_seg16_kernel       QKV in that style with 16 rows per workgroup (8 dims and their
+//                        rotate-half partners) when the 32-row groups outnumber the CUs.
 // splitk_seg_kernel      down (N = d) for up to 16 prompts in that style: 32 rows x a K
 //                        split per workgroup, float32 partial sums per split.
 // skinny_gemm_kernel     O, and down for more prompts (N = d, too few rows for one
@@ -455,6 +457,38 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(const bf16* __restrict
     }
 }
 
+// RoPE (query and key heads) and the stores of one prompt m's dims i .. i + 3 (a) and their
+// rotate-half partners i + 64 .. + 67 (b) of QKV output head `head`: queries to q, keys and
+// values appended to the caches at row slot_kv[m].
+__device__ __forceinline__ void qkv_pair_store(int head, int i, int m, const f32x4& a, const f32x4& b,
+                                               const ppk::QkvOut& qo) {
+    const bool rotate = head < qo.H + qo.Hkv;
+    bf16x4 lo, hi;
+    if (rotate) {
+        const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float2 t = cs[e];
+            lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
+            hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            lo[e] = static_cast<bf16>(a[e]);
+            hi[e] = static_cast<bf16>(b[e]);
+        }
+    }
+    bf16* dst;
+    if (head < qo.H)
+        dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
+    else
+        dst = static_cast<bf16*>(rotate ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
+              (head - qo.H - (rotate ? 0 : qo.Hkv)) * 128;
+    *reinterpret_cast<bf16x4*>(dst + i) = lo;
+    *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+}
+
 // The rowpair epilogue for prompt m and the 4 rows c .. c + 3 of each of the workgroup's two
 // 16-row blocks: a = block 0's sums, b = block 1's.
 template <int EPI>
@@ -466,33 +500,7 @@ __device__ __forceinline__ void rowpair_epilogue(int g, int m, int c, const f32x
         for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(silu(a[e]) * b[e]);
         *reinterpret_cast<bf16x4*>(static_cast<bf16*>(ep.out) + int64_t(m) * ep.ldo + 16 * g + c) = o;
     } else {                         // QKV: dims i .. i + 3 (a) and i + 64 .. (b) of head g / 4
-        const ppk::QkvOut& qo = ep.qkv;
-        const int head = g >> 2, i = 16 * (g & 3) + c;
-        const bool rotate = head < qo.H + qo.Hkv;
-        bf16x4 lo, hi;
-        if (rotate) {
-            const float2* cs = qo.table + int64_t(qo.slot_pos[m]) * 64 + i;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float2 t = cs[e];
-                lo[e] = static_cast<bf16>(a[e] * t.x - b[e] * t.y);
-                hi[e] = static_cast<bf16>(b[e] * t.x + a[e] * t.y);
-            }
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                lo[e] = static_cast<bf16>(a[e]);
-                hi[e] = static_cast<bf16>(b[e]);
-            }
-        }
-        bf16* dst;
-        if (head < qo.H)
-            dst = static_cast<bf16*>(qo.q) + int64_t(m) * qo.ldq + head * 128;
-        else
-            dst = static_cast<bf16*>(rotate ? qo.kc : qo.vc) + int64_t(qo.slot_kv[m]) * qo.ldkv +
-                  (head - qo.H - (rotate ? 0 : qo.Hkv)) * 128;
-        *reinterpret_cast<bf16x4*>(dst + i) = lo;
-        *reinterpret_cast<bf16x4*>(dst + i + 64) = hi;
+        qkv_pair_store(g >> 2, 16 * (g & 3) + c, m, a, b, ep.qkv);
     }
 }
 
@@ -684,6 +692,103 @@ __global__ __launch_bounds__(256, 2) void rowpair_seg_kernel(const bf16* __restr
             rowpair_epilogue<EPI>(g, m, c, a, b, ep);
         }
     }
+}
+
+// The QKV projection for up to 16 prompts at K = 512 NSEG with 16 weight rows per workgroup:
+// dims i0 .. i0 + 7 of a head (chunk rows 0-7) and their rotate-half partners i0 + 64 ..
+// (rows 8-15).  A 7B layer's 384 groups of 32 rows become 768 workgroups, three on every CU,
+// where 32-row workgroups left half the CUs with two and half with one and the busier half
+// set the time.  One 16-row x 512-column chunk per K segment through the LDS ring and XCD
+// stagger of rowpair_seg_kernel; lane l + 32 holds the partners of lane l's rows, exchanged
+// by a lane swap before the RoPE.
+template <int NSEG, int NW>
+__global__ __launch_bounds__(256, 2) void qkv_seg16_kernel(const bf16* __restrict__ A, int64_t lda, int k,
+                                                           const bf16* __restrict__ W, int64_t ldw,
+                                                           ppk::QkvOut qo) {
+    static_assert(NW >= 2 && NW * RS_CHUNK_B >= 4 * 64 * 16, "ring, and room for the reduction");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lr = lane & 15, q4 = lane >> 4;
+    const int g = blockIdx.x;
+    const int head = g >> 3, i0 = 8 * (g & 7);
+    const int rlo = head * 128 + i0;            // rows rlo .. rlo + 7 and rlo + 64 .. rlo + 71
+    const int rot = (g >> 3) & (NSEG - 1);      // see rowpair_seg_kernel
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>(W + int64_t(rlo) * ldw), 0, static_cast<int>((71 * ldw + RS_COLS * NSEG) * 2), kRsrcWord3);
+    auto issue = [&](int c) {                   // segment c (clamped) into slot c % NW
+        const int sg = ((c < NSEG ? c : NSEG - 1) + rot) & (NSEG - 1);
+        char* slot = smem + (c % NW) * RS_CHUNK_B;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int r = 4 * w + t;
+            const int row = r < 8 ? r : 56 + r;     // 64 + (r - 8)
+            const int soff = static_cast<int>((int64_t(row) * ldw + sg * RS_COLS) * 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, (lds_void*)(slot + r * 1024), 16, 16 * (lane ^ rs_swz(r)),
+                                                     soff, 0, 0);
+        }
+    };
+#pragma unroll
+    for (int c = 0; c < NW - 1; ++c) issue(c);
+    __builtin_amdgcn_sched_barrier(0);
+    const bf16* arow = A + int64_t(min(lr, k - 1)) * lda + 128 * w + 8 * q4;
+    bf16x8 pf[NSEG][4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) pf[0][st] = *reinterpret_cast<const bf16x8*>(arow + rot * RS_COLS + 32 * st);
+    f32x4 acc = {};
+#pragma unroll
+    for (int c = 0; c < NSEG; ++c) {
+        // segment c is in when at most the loads of segments c + 1 .. c + NW - 2 (4 each) are
+        // pending (later register loads only make the wait stricter)
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(4 * (NW - 2)));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue(c + NW - 1);                      // into the slot every wavefront finished at c - 1
+        const char* slot = smem + (c % NW) * RS_CHUNK_B;
+        if (c + 1 < NSEG) {
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+                pf[c + 1][st] =
+                    *reinterpret_cast<const bf16x8*>(arow + ((c + 1 + rot) & (NSEG - 1)) * RS_COLS + 32 * st);
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            const bf16x8 wf = *reinterpret_cast<const bf16x8*>(slot + lr * 1024 +
+                                                               16 * ((16 * w + 4 * st + q4) ^ rs_swz(lr)));
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, pf[c][st], acc, 0, 0, 0);
+        }
+    }
+    // the clamped loads past the last segment land before the ring's LDS is reused
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+    __syncthreads();
+    f32x4* red = reinterpret_cast<f32x4*>(smem);   // [w][lane]
+    red[w * 64 + lane] = acc;
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const int l = threadIdx.x, m = l & 15;
+        f32x4 a = red[l];
+#pragma unroll
+        for (int w2 = 1; w2 < 4; ++w2) a += red[w2 * 64 + l];
+        f32x4 b;                                // rows 8 + 4 (l / 16) ..: the partners, from lane l + 32
+#pragma unroll
+        for (int e = 0; e < 4; ++e) b[e] = __shfl_xor(a[e], 32);
+        if (l < 32 && m < k) qkv_pair_store(head, i0 + 4 * (l >> 4), m, a, b, qo);
+    }
+}
+
+template <int NSEG, int NW>
+void launch_qkv_seg16(int N, hipStream_t s, const bf16* A, int64_t lda, int k, const bf16* W, int64_t ldw,
+                      const ppk::QkvOut& qo) {
+    constexpr int lds = NW * RS_CHUNK_B;
+    static bool attr = [] {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&qkv_seg16_kernel<NSEG, NW>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        return true;
+    }();
+    (void)attr;
+    qkv_seg16_kernel<NSEG, NW><<<N / 16, 256, lds, s>>>(A, lda, k, W, ldw, qo);
 }
 
 template <int EPI, int NSEG, int NW>
@@ -1083,6 +1188,14 @@ void decode_gemm(int epi, const void* A, int64_t lda, int k, const void* W, int6
         return;
     }
     if (epi == kQkvRope) {
+        // 16-row workgroups when the 32-row groups outnumber the CUs (7B: 384 groups become 768
+        // workgroups, 21.4 -> 20.5 us); with fewer groups (Mistral-7B and 1.3B: 192) the 32-row
+        // kernel is faster (16 rows: 2.6% and 3.7% slower steps)
+        if (k <= 16 && (K == 2048 || K == 4096) && N / 32 > 256) {
+            if (K == 4096) launch_qkv_seg16<8, 3>(N, s, a, lda, k, w, ldw, ep.qkv);
+            else launch_qkv_seg16<4, 3>(N, s, a, lda, k, w, ldw, ep.qkv);
+            return;
+        }
         if (!launch_rowpair_seg_for<kQkvRope>(N, K, s, a, lda, k, w, ldw, ep))
             launch_rowpair<kQkvRope>(nmb, N, s, a, lda, k, w, ldw, K, ep);
         return;
