@@ -122,6 +122,7 @@ def _bf16_case(model_name, lengths, n_layers, seed=0):
     ("mistral-7b", [3, 8, 1, 20] * 16, 1, 2),                        # 64 prompts, d 4096: 96 KB staged slice
     ("d5120", [37, 1, 300, 5], 1, 3),                                 # d 5120
     ("llama2-7b", [37, 1, 300, 5], 1, 3),                             # F 11008: down ends in half a 1 KB segment
+    ("llama2-7b", [3] * 15 + [200], 1, 2),                            # 16 prompts: the 1 KB-segment kernels' limit
 ])
 def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     case = _bf16_case(model_name, lengths, n_layers)
