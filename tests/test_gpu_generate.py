@@ -100,7 +100,9 @@ def test_fp32_generate_matches_oracle(lengths, n_new, n_layers):
 
 # ----------------------------------------------------------------------------- bf16, teacher-forced
 # a width past 4096 (the fused residual norm's 8-elements-per-thread form), 13B-like
-WIDE = {"d5120": dict(d_model=5120, n_heads=40, n_kv_heads=40, ffn_dim=13824)}
+WIDE = {"d5120": dict(d_model=5120, n_heads=40, n_kv_heads=40, ffn_dim=13824),
+        # F = 5248 = 10 x 512 + 128: the down projection's last 1 KB segment holds 128 columns
+        "f5248": dict(d_model=2048, n_heads=16, n_kv_heads=16, ffn_dim=5248)}
 
 
 def _bf16_case(model_name, lengths, n_layers, seed=0):
@@ -123,6 +125,7 @@ def _bf16_case(model_name, lengths, n_layers, seed=0):
     ("d5120", [37, 1, 300, 5], 1, 3),                                 # d 5120
     ("llama2-7b", [37, 1, 300, 5], 1, 3),                             # F 11008: down ends in half a 1 KB segment
     ("llama2-7b", [3] * 15 + [200], 1, 2),                            # 16 prompts: the 1 KB-segment kernels' limit
+    ("f5248", [9, 130, 1], 1, 2),
 ])
 def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
     case = _bf16_case(model_name, lengths, n_layers)
