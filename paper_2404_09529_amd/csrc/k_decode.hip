@@ -290,7 +290,7 @@ __device__ __forceinline__ int2 attn_item(int item, int k, int n_gen_chunks, int
 // prompt n_ctx_chunks + n_gen_chunks of them (those past its keys return at once).
 // list != 0: workgroup (g, y) takes the work-list items y, y + gridDim.y, ... of head g (one
 // each when the grid holds them all), so only real chunks occupy the CUs: a batch of nine
-// 1-token prompts and one of 1000 at the 7B shape, 10.4 -> 9.6 us.  The host takes the list
+// 1-token prompts and one of 1000 at the 7B shape, 10.4 -> 10.0 us.  The host takes the list
 // when it is shorter; in the full-batching layout it is not, and the lookup would cost each
 // workgroup a dependent load (1.3B: 2% of the step).  bf16 with one query head per key/value
 // head: four workgroups per CU (at most 128 registers), as the chunks are latency-bound (at
