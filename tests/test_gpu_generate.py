@@ -177,16 +177,18 @@ def test_bf16_decode_steps_teacher_forced(model_name, lengths, n_layers, n_new):
 
 
 # ----------------------------------------------------------------------------- layouts and entry points agree
-@pytest.mark.parametrize("model_name,lengths,n_layers", [
-    ("llama-1.3b", [1, 300, 7, 129, 1, 64], 1),
-    ("mistral-7b", [700, 2, 33], 1),
-    ("d5120", [2, 150, 9], 1),
-    ("llama2-7b", [2, 150, 9, 1], 1),
+@pytest.mark.parametrize("model_name,lengths,n_layers,n_new", [
+    ("llama-1.3b", [1, 300, 7, 129, 1, 64], 1, 5),
+    ("mistral-7b", [700, 2, 33], 1, 5),
+    ("d5120", [2, 150, 9], 1, 5),
+    ("llama2-7b", [2, 150, 9, 1], 1, 5),
+    # past 128 generated tokens: two chunks of generated keys per prompt (the packed layout's
+    # attention work list against the full-batching layout's direct grid)
+    ("llama-1.3b", [3, 260, 1, 40], 1, 140),
 ])
-def test_packed_and_padded_generation_are_bit_identical(model_name, lengths, n_layers):
+def test_packed_and_padded_generation_are_bit_identical(model_name, lengths, n_layers, n_new):
     case = _bf16_case(model_name, lengths, n_layers, seed=1)
     lm_head = W.draw_lm_head(case.wl, 1, case.shape)
-    n_new = 5
     model, pre, lm, first = _prefill(case, lm_head)
     packed = pp.Generation(model, pre, case.lengths, n_new)
     padded = pp.Generation(model, pre, case.lengths, n_new, padded=True)
