@@ -830,8 +830,8 @@ bool launch_rowpair_seg_for(int N, int K, hipStream_t s, const bf16* A, int64_t 
 // part[s][m][n] for residual_rmsnorm to add in split order.  When K ends in part of a segment
 // (K % 512 = 128, 256 or 384), the 16-byte pieces past K of that segment's rows read pieces
 // inside it instead and the prompt columns past K are zeros, so those weights add exact
-// zeros.  Chunks past a short split's segments re-read its first one (in bounds, never
-// used), which keeps 4 loads per chunk step for the fixed wait counts.
+// zeros.  Chunks past a short split's segments re-read its last one (in bounds, never used,
+// and just loaded: L2 hits), which keeps 4 loads per chunk step for the fixed wait counts.
 template <int S, int NW>
 __global__ __launch_bounds__(256, 2) void splitk_seg_kernel(const bf16* __restrict__ A, int64_t lda, int k,
                                                             const bf16* __restrict__ W, int64_t ldw, int N, int K,
@@ -853,7 +853,7 @@ __global__ __launch_bounds__(256, 2) void splitk_seg_kernel(const bf16* __restri
     const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<bf16*>(W + int64_t(r0) * ldw), 0, static_cast<int>((31 * ldw + K) * 2), kRsrcWord3);
     auto seg_of = [&](int sl) {               // the segment the split's sl-th chunk pair reads
-        if (sl >= n_here) return s_lo;
+        if (sl >= n_here) sl = n_here - 1;    // past a short split: its last segment, still in L2
         const int p = sl + rot;
         return s_lo + (p >= n_here ? p - n_here : p);
     };
