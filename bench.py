@@ -16,7 +16,8 @@ Prints one JSON line:
   roofline         the dominant kernel (the gate/up projection GEMM with SwiGLU epilogue),
                    timed live with HIP events on its stream, against the bf16 MFMA peak;
                    `traffic` is its HBM bytes per launch from the committed counter summary,
-                   reported only while the kernel source still matches the one measured
+                   reported only for the workload and seed it was measured on and while the
+                   kernel source still matches the one measured (null otherwise)
   cpu_baseline     the CPU oracle (float32) timed on a stratified sample of the same batch that
                    includes its longest prompt, extrapolated to the whole batch by FLOP
   device_memory    workspace, outputs and peak device memory of packed and padded prefill
@@ -143,14 +144,18 @@ def source_sha256(path):
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def recorded_traffic():
+def recorded_traffic(workload, seed):
     """HBM bytes per launch of the gate/up GEMM from the committed counter summary (a line
-    `record: {json}`), or None when there is none or the kernel source has changed since."""
+    `record: {json}`), or None when there is none, when it was taken on another workload or
+    seed (the re-fetches depend on the plan's shape), or when the kernel source has changed
+    since."""
     try:
         with open(TRAFFIC_SUMMARY) as f:
             line = next(l for l in f if l.startswith("record: "))
         rec = json.loads(line[len("record: "):])
     except (OSError, StopIteration, ValueError):
+        return None
+    if rec.get("workload") != workload or rec.get("seed") != seed:
         return None
     if rec.get("kernel_source_sha256") != source_sha256(GEMM_SOURCE):
         return None
@@ -193,8 +198,8 @@ def traffic_pass(args):
     torch.cuda.synchronize()
     del A, Wgu, C
     calibration_copy()
-    print(json.dumps({"traffic_pass": wl.name, "gemm_launches": args.kernel_launches, "T": T, "d": d, "F": F,
-                      "total_len": int(lengths.sum()), "copy_read_bytes": COPY_BYTES,
+    print(json.dumps({"traffic_pass": wl.name, "seed": args.seed, "gemm_launches": args.kernel_launches,
+                      "T": T, "d": d, "F": F, "total_len": int(lengths.sum()), "copy_read_bytes": COPY_BYTES,
                       "copy_write_bytes": COPY_BYTES, "kernel_source_sha256": source_sha256(GEMM_SOURCE)}),
           flush=True)
 
@@ -782,7 +787,7 @@ def main():
     achieved = k_flops / (kt["ms_mean"] / 1e3) / 1e12
     del A, Cb
     log(f"gate/up GEMM: {kt['ms_mean']:.3f} ms/launch, {achieved:.1f} TFLOP/s algorithmic")
-    traffic = recorded_traffic() if bf else None   # A, W once; C written once (k_bytes)
+    traffic = recorded_traffic(case.wl.name, args.seed) if bf else None   # A, W once; C written once (k_bytes)
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
