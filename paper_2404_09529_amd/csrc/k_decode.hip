@@ -977,9 +977,11 @@ void launch_rowpair(int nmb, int N, hipStream_t s, const bf16* A, int64_t lda, i
 
 // Residual add of a split-K projection fused with the RMSNorm that follows it, one workgroup
 // of d / (4 E) threads per prompt row, 4 E consecutive elements per thread (E = 1 up to
-// d = 4096, 2 up to 8192): x[m] += sum over splits of part[.][m] (split order; the loads of 4
-// splits issued together), stored back; then out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * g.
-// S = 0: no pending projection.
+// d = 4096, 2 up to 8192): x[m] += sum over splits of part[.][m], added in split order, stored
+// back; then out[m] = x[m] / sqrt(mean(x[m]^2) + eps) * g.  S = 0: no pending projection.
+// The kernel is latency-bound (k workgroups, a few KB each), so everything it reads (the row,
+// the gains, up to 8 splits' partial sums) is issued before the first wait: one memory round
+// trip where S <= 8 rather than one per split.
 template <typename TO, int E>
 __global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ part,
                                                                 int S, int k, int d, const float* __restrict__ g,
@@ -987,27 +989,28 @@ __global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restric
     __shared__ float red[16];
     const int m = blockIdx.x, c = 4 * E * threadIdx.x;
     float* xr = x + int64_t(m) * d + c;
-    f32x4 v[E];
+    f32x4 v[E], gg[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) v[e] = *reinterpret_cast<const f32x4*>(xr + 4 * e);
+    for (int e = 0; e < E; ++e) {
+        v[e] = *reinterpret_cast<const f32x4*>(xr + 4 * e);
+        gg[e] = *reinterpret_cast<const f32x4*>(g + c + 4 * e);
+    }
     if (S > 0) {
         const float* p = part + int64_t(m) * d + c;
         const int64_t stride = int64_t(k) * d;
-        int s = 0;
-        for (; s + 4 <= S; s += 4) {
-            f32x4 a[4][E];
+        for (int s = 0; s < S; s += 8) {
+            f32x4 a[8][E];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < 8; ++u)
+                if (s + u < S)
 #pragma unroll
-                for (int e = 0; e < E; ++e) a[u][e] = *reinterpret_cast<const f32x4*>(p + (s + u) * stride + 4 * e);
+                    for (int e = 0; e < E; ++e) a[u][e] = *reinterpret_cast<const f32x4*>(p + (s + u) * stride + 4 * e);
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < 8; ++u)
+                if (s + u < S)
 #pragma unroll
-                for (int e = 0; e < E; ++e) v[e] += a[u][e];
+                    for (int e = 0; e < E; ++e) v[e] += a[u][e];
         }
-        for (; s < S; ++s)
-#pragma unroll
-            for (int e = 0; e < E; ++e) v[e] += *reinterpret_cast<const f32x4*>(p + s * stride + 4 * e);
 #pragma unroll
         for (int e = 0; e < E; ++e) *reinterpret_cast<f32x4*>(xr + 4 * e) = v[e];
     }
@@ -1025,14 +1028,13 @@ __global__ __launch_bounds__(1024) void residual_rmsnorm_kernel(float* __restric
     const float r = rsqrtf(tot / static_cast<float>(d) + eps);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const f32x4 gg = *reinterpret_cast<const f32x4*>(g + c + 4 * e);
         if constexpr (sizeof(TO) == 2) {
             bf16x4 o;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) o[i] = static_cast<bf16>(v[e][i] * r * gg[i]);
+            for (int i = 0; i < 4; ++i) o[i] = static_cast<bf16>(v[e][i] * r * gg[e][i]);
             *reinterpret_cast<bf16x4*>(out + int64_t(m) * d + c + 4 * e) = o;
         } else {
-            *reinterpret_cast<f32x4*>(out + int64_t(m) * d + c + 4 * e) = v[e] * r * gg;
+            *reinterpret_cast<f32x4*>(out + int64_t(m) * d + c + 4 * e) = v[e] * r * gg[e];
         }
     }
 }
