@@ -45,6 +45,7 @@ METRIC = "effective prefill tokens/s + TFLOP/s (% bf16 MFMA peak) vs padded pref
 GEMM_SOURCE = os.path.join(ROOT, "paper_2404_09529_amd", "csrc", "k_gemm_bf16.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_swiglu_llama2-7b-lognormal_traffic.md")
 COPY_BYTES = 1 << 30        # the calibration copy reads and writes 1 GiB
+CPU_SAMPLE_S = 12.0         # about this much timed oracle work for cpu_baseline (more layers while it fits)
 
 
 def log(msg):
@@ -230,10 +231,11 @@ def cpu_baseline(case):
 
     The prompts are split by length into four quartiles; from each the prompt of median
     length is timed, and from the top quartile also the batch's longest prompt.  Each is
-    timed through one decoder layer (the oracle's per-layer work is the same in every
-    layer, so n layers take n times as long); a quartile's time is its sampled prompts' time
-    scaled by the quartile's FLOP over theirs.  The embedding and final norm are left out
-    (no FLOP)."""
+    timed through one decoder layer, then, while the timing stays near CPU_SAMPLE_S in all,
+    through as many of the model's other layers as fit (the oracle's per-layer work is the
+    same in every layer, so a quartile's per-layer time is the mean over the layers run, and
+    n layers take n times that); a quartile's time is then scaled by its FLOP over its
+    sampled prompts'.  The embedding and final norm are left out (no FLOP)."""
     import dataclasses
 
     import numpy as np
@@ -250,29 +252,43 @@ def cpu_baseline(case):
     order = np.argsort(lengths, kind="stable")
     strata = [q for q in np.array_split(order, 4) if len(q)]
     longest = int(order[-1])
-    total_s, timed, t_all = 0.0, [], time.perf_counter()
+    picks = []
+    for qi, q in enumerate(strata):
+        picks.append([int(q[len(q) // 2])])
+        if qi == len(strata) - 1 and longest not in picks[-1]:
+            picks[-1].append(longest)
+
+    def run(layers):                  # seconds per quartile for its picks through `layers`
+        el = []
+        for p in picks:
+            t = time.perf_counter()
+            for i in p:
+                D.prefill_prompt(case.tokens[off[i]:off[i + 1]], case.weights, layers, dtype=np.float32)
+            el.append(time.perf_counter() - t)
+        return el
+
+    t_all = time.perf_counter()
     with threadpool_limits(limits=threads):
         D.prefill_prompt(case.tokens[off[0]:off[0] + min(16, int(lengths[0]))], case.weights, one,
                          dtype=np.float32)                      # warm-up
-        for qi, q in enumerate(strata):
-            picks = [int(q[len(q) // 2])]
-            if qi == len(strata) - 1 and longest not in picks:
-                picks.append(longest)
-            t = time.perf_counter()
-            for i in picks:
-                D.prefill_prompt(case.tokens[off[i]:off[i + 1]], case.weights, one, dtype=np.float32)
-            el = time.perf_counter() - t
-            f_sample = sum(prompt_flops(shape, int(lengths[i])) for i in picks)
-            f_stratum = sum(prompt_flops(shape, int(lengths[i])) for i in q)
-            total_s += el * f_stratum / f_sample * shape.n_layers
-            timed += [(int(i), int(lengths[i])) for i in picks]
+        el = run(one)
+        first = time.perf_counter() - t_all
+        extra = int(min(shape.n_layers - 1, max(0.0, CPU_SAMPLE_S / max(first, 1e-9) - 1.0)))
+        if extra:
+            el = [a + b for a, b in zip(el, run(dataclasses.replace(shape, n_layers=extra)))]
     wall = time.perf_counter() - t_all
+    total_s, timed = 0.0, []
+    for q, p, e in zip(strata, picks, el):
+        f_sample = sum(prompt_flops(shape, int(lengths[i])) for i in p)
+        f_stratum = sum(prompt_flops(shape, int(lengths[i])) for i in q)
+        total_s += e / (1 + extra) * f_stratum / f_sample * shape.n_layers
+        timed += [(int(i), int(lengths[i])) for i in p]
     L = int(lengths.sum())
     return {"value": L / total_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "cpu_model": cpu_model(), "affinity_cpus": affinity, "dtype": "f32",
             "extrapolated_batch_s": round(total_s, 2),
             "sample": f"stratified: the median-length prompt of each length quartile plus the longest prompt, "
-                      f"{len(timed)} prompts (ids, lengths) {timed}, each through 1 of the {shape.n_layers} "
+                      f"{len(timed)} prompts (ids, lengths) {timed}, each through {1 + extra} of the {shape.n_layers} "
                       f"layers; whole batch ({len(lengths)} prompts, {L} tokens, {shape.n_layers} layers) "
                       f"extrapolated by algorithmic FLOP per quartile; float32 numpy oracle on {threads} "
                       f"threads; {wall:.1f} s timed"}
