@@ -123,6 +123,7 @@ def _bf16_case(model_name, lengths, n_layers, seed=0):
     ("llama-1.3b", [2, 11, 6, 1] * 16, 1, 2),                        # 64 prompts: four blocks
     ("mistral-7b", [3, 8, 1, 20] * 16, 1, 2),                        # 64 prompts, d 4096: 96 KB staged slice
     ("d5120", [37, 1, 300, 5], 1, 3),                                 # d 5120
+    ("d5120", [4, 9, 1, 33] * 5, 1, 2),                               # d 5120, 20 prompts: 18 down splits
     ("llama2-7b", [37, 1, 300, 5], 1, 3),                             # F 11008: down ends in half a 1 KB segment
     ("llama2-7b", [3] * 15 + [200], 1, 2),                            # 16 prompts: the 1 KB-segment kernels' limit
     ("f5248", [9, 130, 1], 1, 2),
