@@ -25,7 +25,7 @@ cache and generating the first token; section 4.3 adds the unpacking): for
 every prompt, the logits of its last token, hidden[last] W_lm^T over the
 vocabulary, and the greedy choice argmax, lowest id on ties (``first_token``).
 
-Readings of the paper (each listed with its reason in the design doc):
+Readings of the paper, where it is silent or ambiguous:
 * the score scale is 1/sqrt(D), D the head size (the paper writes the
   single-head form with the model width);
 * the mask is applied to the scores before the softmax, masked entries

@@ -18,7 +18,7 @@ consumes fed token t at position l + t must produce (its key and value, which
 the step appends to the cache, and the final hidden row whose logits choose
 the next token), because causality makes row l + t independent of later rows.
 
-Readings (each listed with its reason in the design doc): generation is greedy; the
+Readings, where the paper is silent: generation is greedy; the
 token consumed by the first decode step is the first token chosen from the
 prefill (section 2.3); positions continue each prompt's own positions, l, l+1,
 ... (restart positions, section 3.2, carried into generation).
